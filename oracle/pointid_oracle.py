@@ -1,0 +1,236 @@
+"""Plain fp64 CPU oracle for per-hit track/shower/Michel classification.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the ``cpu_baseline`` leg of ``bench.py`` may import or call this module.  The
+product path (the HIP library and its Python binding) never touches it, and it
+shares no code with that path: it needs only numpy.
+
+What it computes, with the passage each step follows:
+
+* Patch construction, paper §2.1 (EmTrackMichelId / PointIdAlg): a 48x48 image
+  centred on the hit's wire and peak time, rows indexing the wire and columns
+  the time.  Reading used here: row r, column c of the patch of hit (w, t) is
+  the plane pixel (w - 24 + r, t - 24 + c), and 0 wherever that pixel lies
+  outside the plane.
+* The network of paper §2.2: 48 separate 5x5 filters, stride 1, giving 48 maps
+  of 44x44 (so no padding), ReLU; a fully connected layer of 128 with ReLU; one
+  of 32 with ReLU; then two branches from the 32: three outputs through a
+  softmax and one through a sigmoid.  Dropout is the identity at inference.
+  Readings: the filter is a cross-correlation (no kernel flip), every layer
+  has a bias (the paper's parameter count of 11,900,420 requires all six), and
+  the 44x44x48 maps are flattened channels-last, index (y*44 + x)*48 + k.
+
+All arithmetic is float64 with no intermediate rounding; each output is rounded
+to float32 once at the end.  Matrix products use numpy's ``@`` (a library
+primitive) with no blocking or reordering of our own.  Large inputs are
+processed in chunks of hits; chunking never changes a result bit because every
+hit is computed independently.
+
+Pins: ``tests/test_oracle.py`` checks each function against facts fixed by the
+paper or by mathematics (hand-computed patch coordinates, brute-force
+convolution, a library convolution, closed forms of the heads, the parameter
+count, invariances).  The physical meaning of the scores (trained weights on
+ProtoDUNE-SP data) is parity unpinned: neither exists here.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+PATCH = 48                 # patch side, paper §2.1
+HALF = PATCH // 2          # the hit sits at patch pixel (24, 24)
+KS = 5                     # filter side, paper §2.2
+NCH = 48                   # number of filters, paper §2.2
+FM = PATCH - KS + 1        # 44: map side of a stride-1 unpadded 5x5 filter
+FC1_IN = FM * FM * NCH     # 92,928
+FC1_OUT = 128
+FC2_OUT = 32
+NCLS = 3
+
+CHUNK = 256
+
+
+# --------------------------------------------------------------------------
+# Patch construction (paper §2.1)
+# --------------------------------------------------------------------------
+
+def gather_patches(image, hits) -> np.ndarray:
+    """float32 [n][48][48]: P[r][c] = image[w-24+r][t-24+c], 0 outside the plane.
+
+    ``image`` is [n_wires][n_ticks]; ``hits`` is int [n][2] = (wire, tick).
+    The values are copied, never computed, so the result is exact.
+    """
+    image = np.asarray(image, dtype=np.float32)
+    hits = np.asarray(hits, dtype=np.int64).reshape(-1, 2)
+    W, T = image.shape
+    n = hits.shape[0]
+    rows = hits[:, 0:1] - HALF + np.arange(PATCH)[None, :]      # [n][48] wires
+    cols = hits[:, 1:2] - HALF + np.arange(PATCH)[None, :]      # [n][48] ticks
+    inside = ((rows >= 0) & (rows < W))[:, :, None] & ((cols >= 0) & (cols < T))[:, None, :]
+    vals = image[np.clip(rows, 0, W - 1)[:, :, None], np.clip(cols, 0, T - 1)[:, None, :]]
+    out = np.where(inside, vals, np.float32(0.0)).astype(np.float32)
+    return out.reshape(n, PATCH, PATCH)
+
+
+def gather_patches_planes(images, hits3) -> np.ndarray:
+    """Multi-plane gather: ``hits3`` is int [n][3] = (plane, wire, tick).
+
+    A plane index outside [0, len(images)) gives an all-zero patch.
+    """
+    hits3 = np.asarray(hits3, dtype=np.int64).reshape(-1, 3)
+    out = np.zeros((hits3.shape[0], PATCH, PATCH), np.float32)
+    for p, img in enumerate(images):
+        sel = np.nonzero(hits3[:, 0] == p)[0]
+        if sel.size:
+            out[sel] = gather_patches(img, hits3[sel, 1:3])
+    return out
+
+
+def to_bf16_rne(x) -> np.ndarray:
+    """Round float32 values to bfloat16 (round to nearest, ties to even).
+
+    Returned as float32 holding exactly the bfloat16 value.  Finite inputs only.
+    A bfloat16 keeps the top 16 bits of the float32 encoding; the discarded low
+    16 bits decide the rounding: above half rounds up, below half down, exactly
+    half rounds to the neighbour whose last kept bit is 0.
+    """
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    low = b & 0xFFFF
+    keep = b >> 16
+    up = (low > 0x8000) | ((low == 0x8000) & ((keep & 1) == 1))
+    keep = keep + up.astype(np.uint64)
+    return (keep << 16).astype(np.uint32).view(np.float32).reshape(np.shape(x))
+
+
+def bf16_bits(x) -> np.ndarray:
+    """uint16 bit patterns of ``to_bf16_rne(x)``."""
+    return (to_bf16_rne(x).view(np.uint32) >> 16).astype(np.uint16)
+
+
+# --------------------------------------------------------------------------
+# The network (paper §2.2)
+# --------------------------------------------------------------------------
+
+def conv_relu(patches, conv_w, conv_b) -> np.ndarray:
+    """48 maps of 44x44 per patch, channels-last: A[n][y][x][k] (float64).
+
+    A[y][x][k] = ReLU(b_k + sum_{u,v<5} K[k][u][v] * P[y+u][x+v]): a stride-1
+    cross-correlation over the valid region.  The 25 taps of every output are
+    laid out by a sliding-window view (no arithmetic), then contracted with the
+    filters by one matrix product.
+    """
+    P = np.asarray(patches, dtype=np.float64).reshape(-1, PATCH, PATCH)
+    K = np.asarray(conv_w, dtype=np.float64).reshape(NCH, KS * KS)
+    win = np.lib.stride_tricks.sliding_window_view(P, (KS, KS), axis=(1, 2))
+    taps = win.reshape(P.shape[0], FM, FM, KS * KS)         # [n][y][x][u*5+v]
+    pre = taps @ K.T + np.asarray(conv_b, dtype=np.float64)  # [n][y][x][k]
+    return np.maximum(pre, 0.0)
+
+
+def flatten_hwc(A) -> np.ndarray:
+    """[n][44][44][48] -> [n][92928] with index (y*44 + x)*48 + k."""
+    return np.asarray(A).reshape(A.shape[0], FC1_IN)
+
+
+def dense_relu(x, w, b) -> np.ndarray:
+    """ReLU(b + x @ W) in float64."""
+    return np.maximum(np.asarray(x, np.float64) @ np.asarray(w, np.float64)
+                      + np.asarray(b, np.float64), 0.0)
+
+
+def softmax(z) -> np.ndarray:
+    """exp(z - max z) / sum exp(z - max z) along the last axis."""
+    z = np.asarray(z, np.float64)
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def sigmoid(q) -> np.ndarray:
+    """1 / (1 + e^-q), evaluated without overflow for either sign of q."""
+    q = np.asarray(q, np.float64)
+    e = np.exp(-np.abs(q))
+    return np.where(q >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+
+
+def heads(h2, weights) -> np.ndarray:
+    """Scores [n][4] float64 = (softmax(cls), sigmoid(mic)) from the 32-wide layer."""
+    z = h2 @ np.asarray(weights["cls_w"], np.float64) + np.asarray(weights["cls_b"], np.float64)
+    q = h2 @ np.asarray(weights["mic_w"], np.float64) + np.asarray(weights["mic_b"], np.float64)[0]
+    return np.concatenate([softmax(z), sigmoid(q)[:, None]], axis=1)
+
+
+def forward(patches, weights, return_hidden: bool = False):
+    """Scores for a batch of patches, float64 [n][4] (no final rounding).
+
+    ``return_hidden`` also returns (A, h1, h2) for diagnostics.
+    """
+    A = conv_relu(patches, weights["conv_w"], weights["conv_b"])
+    a = flatten_hwc(A)
+    h1 = dense_relu(a, weights["fc1_w"], weights["fc1_b"])
+    h2 = dense_relu(h1, weights["fc2_w"], weights["fc2_b"])
+    s = heads(h2, weights)
+    if return_hidden:
+        return s, (A, h1, h2)
+    return s
+
+
+def logits(patches, weights) -> np.ndarray:
+    """Pre-softmax class logits [n][3] (float64), for tie diagnostics."""
+    A = conv_relu(patches, weights["conv_w"], weights["conv_b"])
+    h1 = dense_relu(flatten_hwc(A), weights["fc1_w"], weights["fc1_b"])
+    h2 = dense_relu(h1, weights["fc2_w"], weights["fc2_b"])
+    return h2 @ np.asarray(weights["cls_w"], np.float64) + np.asarray(weights["cls_b"], np.float64)
+
+
+def classify_patches(patches, weights, chunk: int = CHUNK) -> np.ndarray:
+    """float32 [n][4] = (p_track, p_em, p_none, p_michel) for pre-cut patches."""
+    patches = np.asarray(patches, dtype=np.float32).reshape(-1, PATCH, PATCH)
+    n = patches.shape[0]
+    out = np.empty((n, 4), np.float32)
+    for s in range(0, n, chunk):
+        out[s:s + chunk] = forward(patches[s:s + chunk], weights).astype(np.float32)
+    return out
+
+
+def classify(image, hits, weights, chunk: int = CHUNK) -> np.ndarray:
+    """Scores for every hit of one plane, in hit order."""
+    hits = np.asarray(hits).reshape(-1, 2)
+    out = np.empty((hits.shape[0], 4), np.float32)
+    for s in range(0, hits.shape[0], chunk):
+        out[s:s + chunk] = forward(gather_patches(image, hits[s:s + chunk]),
+                                   weights).astype(np.float32)
+    return out
+
+
+def classify_planes(images, hits3, weights, chunk: int = CHUNK) -> np.ndarray:
+    """Scores for (plane, wire, tick) hits over several planes, in hit order."""
+    hits3 = np.asarray(hits3).reshape(-1, 3)
+    out = np.empty((hits3.shape[0], 4), np.float32)
+    for s in range(0, hits3.shape[0], chunk):
+        out[s:s + chunk] = forward(gather_patches_planes(images, hits3[s:s + chunk]),
+                                   weights).astype(np.float32)
+    return out
+
+
+def quantize_bf16_model(weights) -> dict:
+    """Weights as the bf16 path holds them: conv and FC1 filters rounded to
+    bfloat16 (RNE), everything else unchanged.  Diagnostic use only: the
+    bf16 path is graded against the full-precision oracle."""
+    q = dict(weights)
+    q["conv_w"] = to_bf16_rne(weights["conv_w"])
+    q["fc1_w"] = to_bf16_rne(weights["fc1_w"])
+    return q
+
+
+def forward_bf16_emulated(patches, weights) -> np.ndarray:
+    """Diagnostic: the network with the bf16 path's roundings applied (patch,
+    conv filter, conv output and FC1 filter rounded to bfloat16), accumulated in
+    float64.  Localises a bf16-path discrepancy much more tightly than the
+    full-precision oracle; it is not the grading reference."""
+    q = quantize_bf16_model(weights)
+    P = to_bf16_rne(np.asarray(patches, np.float32))
+    A = conv_relu(P, q["conv_w"], q["conv_b"])
+    A = to_bf16_rne(A.astype(np.float32)).astype(np.float64)
+    h1 = dense_relu(flatten_hwc(A), q["fc1_w"], q["fc1_b"])
+    h2 = dense_relu(h1, q["fc2_w"], q["fc2_b"])
+    return heads(h2, q)

@@ -1,0 +1,323 @@
+"""Pins for the CPU oracle: facts fixed by the paper or by mathematics.
+
+Each test checks the oracle against something other than itself: the paper's
+architecture numbers, hand-computed patch coordinates, hand-derived closed
+forms (tests/golden), brute-force loops, torch's own conv2d/linear in float64,
+torch's bfloat16 rounding, and invariances of a per-hit computation.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _zero_model():
+    return {k: np.zeros(s, np.float32) for k, s in synth.WEIGHT_SHAPES.items()}
+
+
+# ---------------------------------------------------------------- architecture
+
+def test_architecture_matches_paper():
+    g = _golden("paper_architecture.json")
+    assert oracle.PATCH == g["patch_side"]
+    assert oracle.NCH == g["filters"] and oracle.KS == g["filter_side"]
+    assert oracle.FM == g["map_side"] == g["patch_side"] - g["filter_side"] + 1
+    assert oracle.FC1_OUT == g["fc1_neurons"] and oracle.FC2_OUT == g["fc2_neurons"]
+    assert oracle.NCLS == g["softmax_outputs"]
+    # the parameter count fixes biases on all six layers and an unpadded conv
+    conv = g["filters"] * (g["filter_side"] ** 2 + 1)
+    fc1 = oracle.FC1_IN * g["fc1_neurons"] + g["fc1_neurons"]
+    fc2 = g["fc1_neurons"] * g["fc2_neurons"] + g["fc2_neurons"]
+    cls = g["fc2_neurons"] * g["softmax_outputs"] + g["softmax_outputs"]
+    mic = g["fc2_neurons"] * g["sigmoid_outputs"] + g["sigmoid_outputs"]
+    assert conv + fc1 + fc2 + cls + mic == g["trainable_parameters"] == 11_900_420
+    assert synth.n_parameters() == g["trainable_parameters"]
+    w = synth.he_normal_weights()
+    assert sum(v.size for v in w.values()) == g["trainable_parameters"]
+
+
+def test_patch_volume_matches_paper():
+    g = _golden("paper_architecture.json")
+    bytes_per_patch = g["patch_side"] ** 2 * g["bits_per_pixel"] // 8
+    assert bytes_per_patch == 9216
+    gbit = g["patches_per_event"] * bytes_per_patch * 8 / 1e9
+    assert abs(gbit - g["gigabits_per_event"]) < 0.05
+    p = oracle.gather_patches(np.zeros((8, 8), np.float32), [[0, 0]])
+    assert p.dtype == np.float32 and p[0].nbytes == bytes_per_patch
+
+
+# ---------------------------------------------------------------- patch gather
+
+def test_patch_coordinates_centre():
+    img = synth.coord_image(128, 512)
+    P = oracle.gather_patches(img, [[64, 256]])[0]
+    r = np.arange(48)[:, None]
+    c = np.arange(48)[None, :]
+    expect = 1 + 1000 * (40 + r) + (232 + c)
+    assert np.array_equal(P, expect.astype(np.float32))
+    assert P[24, 24] == 1 + 1000 * 64 + 256      # the hit sits at (24, 24)
+
+
+def test_patch_corners_zero_padded():
+    W, T = 128, 512
+    img = synth.coord_image(W, T)
+    P = oracle.gather_patches(img, [[0, 0], [W - 1, T - 1]])
+    r = np.arange(48)[:, None]
+    c = np.arange(48)[None, :]
+    lo = np.where((r >= 24) & (c >= 24), 1 + 1000 * (r - 24) + (c - 24), 0)
+    assert np.array_equal(P[0], lo.astype(np.float32))
+    hi = np.where((r <= 24) & (c <= 24),
+                  1 + 1000 * (W - 1 - 24 + r) + (T - 1 - 24 + c), 0)
+    assert np.array_equal(P[1], hi.astype(np.float32))
+
+
+def test_patch_outside_and_off_by_one():
+    W, T = 64, 100
+    img = synth.coord_image(W, T)
+    hits = [[-100, 50], [W + 24, 50], [W + 23, 50], [30, -23], [30, -24], [30, T + 23]]
+    P = oracle.gather_patches(img, hits)
+    assert not P[0].any()
+    assert not P[1].any()                        # centre 24 past the last wire
+    assert P[2][0].all() and not P[2][1:].any()  # only row 0 = wire W-1 inside
+    assert np.array_equal(P[2][0], img[W - 1, 50 - 24:50 + 24])
+    assert P[3][:, 47].all() and not P[3][:, :47].any()   # only column 47 = tick 0
+    assert not P[4].any()
+    assert P[5][:, 0].all() and not P[5][:, 1:].any()
+
+
+def test_multiplane_gather():
+    a = synth.coord_image(30, 70)
+    b = synth.coord_image(50, 60) + 7
+    hits3 = np.array([[1, 5, 5], [0, 29, 69], [2, 3, 3], [-1, 3, 3], [1, 49, 0]])
+    P = oracle.gather_patches_planes([a, b], hits3)
+    assert np.array_equal(P[0], oracle.gather_patches(b, [[5, 5]])[0])
+    assert np.array_equal(P[1], oracle.gather_patches(a, [[29, 69]])[0])
+    assert not P[2].any() and not P[3].any()
+    assert np.array_equal(P[4], oracle.gather_patches(b, [[49, 0]])[0])
+
+
+def test_bf16_rne_matches_torch():
+    rng = np.random.default_rng(0)
+    x = (rng.standard_normal(100000) * 10 ** rng.uniform(-6, 6, 100000)).astype(np.float32)
+    # exact ties with both parities of the kept bit, and values just off a tie
+    base = rng.integers(0x3F800000 >> 16, 0x47000000 >> 16, 2000).astype(np.uint32) << 16
+    ties = np.concatenate([base | 0x8000, base | 0x7FFF, base | 0x8001,
+                           (base | 0x10000) | 0x8000]).view(np.float32)
+    x = np.concatenate([x, ties, -ties, np.float32([0.0, -0.0, 1.0, 65504.0])])
+    ours = oracle.to_bf16_rne(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(ours.view(np.uint32), ref.view(np.uint32))
+    assert np.array_equal(oracle.bf16_bits(x),
+                          (ref.view(np.uint32) >> 16).astype(np.uint16))
+
+
+# ---------------------------------------------------------------- convolution
+
+def _conv_bruteforce(P, K, b):
+    n = P.shape[0]
+    nk = K.shape[0]
+    out = np.zeros((n, 44, 44, nk))
+    for i in range(n):
+        for k in range(nk):
+            for y in range(44):
+                for x in range(44):
+                    s = float(b[k])
+                    for u in range(5):
+                        for v in range(5):
+                            s += float(K[k, u, v]) * float(P[i, y + u, x + v])
+                    out[i, y, x, k] = s if s > 0 else 0.0
+    return out
+
+
+def test_conv_matches_bruteforce_loops():
+    rng = np.random.default_rng(1)
+    P = rng.standard_normal((2, 48, 48)).astype(np.float32) * 3
+    K = rng.standard_normal((3, 5, 5)).astype(np.float32)
+    b = rng.uniform(-1, 1, 3).astype(np.float32)
+    got = oracle.conv_relu(P, np.concatenate([K, np.zeros((45, 5, 5), np.float32)]),
+                           np.concatenate([b, np.zeros(45, np.float32)]))[..., :3]
+    ref = _conv_bruteforce(P, K, b)
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-12)
+
+
+def test_conv_matches_torch_conv2d_fp64():
+    rng = np.random.default_rng(2)
+    P = rng.standard_normal((5, 48, 48)).astype(np.float32) * 4
+    w = synth.he_normal_weights()
+    got = oracle.conv_relu(P, w["conv_w"], w["conv_b"])
+    t = torch.nn.functional.conv2d(torch.from_numpy(P).double()[:, None],
+                                   torch.from_numpy(w["conv_w"]).double()[:, None],
+                                   torch.from_numpy(w["conv_b"]).double())
+    ref = torch.relu(t).permute(0, 2, 3, 1).numpy()       # NCHW -> NHWC
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv_delta_kernel_is_shifted_crop():
+    rng = np.random.default_rng(3)
+    P = rng.standard_normal((3, 48, 48)).astype(np.float32)
+    for (k, u, v) in [(0, 0, 0), (5, 2, 3), (47, 4, 4), (11, 0, 4)]:
+        K = np.zeros((48, 5, 5), np.float32)
+        K[k, u, v] = 1.0
+        A = oracle.conv_relu(P, K, np.zeros(48, np.float32))
+        assert np.array_equal(A[..., k], np.maximum(P[:, u:u + 44, v:v + 44], 0))
+        others = np.delete(A, k, axis=3)
+        assert not others.any()
+
+
+def test_conv_delta_image_gives_unflipped_kernel():
+    K = synth.he_normal_weights()["conv_w"]
+    P = np.zeros((1, 48, 48), np.float32)
+    r0, c0 = 20, 30
+    P[0, r0, c0] = 1.0
+    A = oracle.conv_relu(P, K, np.zeros(48, np.float32))[0]
+    for u in range(5):
+        for v in range(5):
+            np.testing.assert_array_equal(A[r0 - u, c0 - v, :], np.maximum(K[:, u, v], 0))
+
+
+def test_flatten_is_channels_last():
+    A = np.arange(2 * 44 * 44 * 48, dtype=np.float64).reshape(2, 44, 44, 48)
+    a = oracle.flatten_hwc(A)
+    for (y, x, k) in [(0, 0, 0), (3, 7, 11), (43, 43, 47), (10, 0, 5)]:
+        assert a[1, (y * 44 + x) * 48 + k] == A[1, y, x, k]
+
+
+# ---------------------------------------------------------------- dense + heads
+
+def test_dense_selector_closed_form():
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((6, 10))
+    W = np.zeros((10, 4))
+    W[3, 0] = 1.0
+    W[7, 2] = -2.0
+    b = np.array([0.5, -0.25, 0.0, 1.0])
+    got = oracle.dense_relu(x, W, b)
+    np.testing.assert_array_equal(got[:, 0], np.maximum(x[:, 3] + 0.5, 0))
+    np.testing.assert_array_equal(got[:, 1], np.zeros(6))
+    np.testing.assert_array_equal(got[:, 2], np.maximum(-2.0 * x[:, 7], 0))
+    np.testing.assert_array_equal(got[:, 3], np.ones(6))
+
+
+def test_zero_weight_model_closed_form():
+    g = _golden("closed_forms.json")["zero_weights"]
+    w = _zero_model()
+    w["cls_b"] = np.float32([0.0, math.log(2), math.log(3)])
+    w["mic_b"] = np.float32([math.log(3)])
+    rng = np.random.default_rng(5)
+    P = rng.standard_normal((4, 48, 48)).astype(np.float32) * 10
+    s = oracle.classify_patches(P, w)
+    expect = [eval(e, {}, {}) for e in g["expected"]]        # "1/6", ...
+    # cls_b/mic_b are float32 roundings of ln 2, ln 3: 1e-7 relative slack
+    np.testing.assert_allclose(s, np.tile(expect, (4, 1)), rtol=2e-7, atol=0)
+
+
+def test_softmax_and_sigmoid_properties():
+    rng = np.random.default_rng(6)
+    z = rng.standard_normal((1000, 3)) * 30
+    s = oracle.softmax(z)
+    assert np.all(np.abs(s.sum(1) - 1) <= 1e-12)
+    assert np.all(np.argmax(s, 1) == np.argmax(z, 1))
+    q = np.concatenate([rng.standard_normal(1000) * 20, [-1000.0, 1000.0, 0.0]])
+    m = oracle.sigmoid(q)
+    assert np.all((m >= 0) & (m <= 1)) and np.all(np.isfinite(m))
+    assert m[-1] == 0.5 and m[-2] == 1.0 and m[-3] == 0.0
+    inner = np.abs(q) < 30
+    assert np.all((m[inner] > 0) & (m[inner] < 1))
+    np.testing.assert_allclose(oracle.sigmoid(q[:1000]), 1 / (1 + np.exp(-q[:1000])), rtol=1e-15)
+
+
+def test_single_pixel_chains_closed_form():
+    g = _golden("closed_forms.json")["single_pixel_chains"]
+    W, T = g["plane"]
+    e = math.e
+    hit_scores = [e / (e + 1 + 1 / e), 1 / (e + 1 + 1 / e), (1 / e) / (e + 1 + 1 / e), e / (1 + e)]
+    miss_scores = [1 / 3, 1 / 3, 1 / 3, 0.5]
+    for case in g["cases"]:
+        img = np.zeros((W, T), np.float32)
+        img[case["pixel"][0], case["pixel"][1]] = 1.0
+        w = _zero_model()
+        k, u, v = case["tap"]
+        w["conv_w"][k, u, v] = 1.0
+        fy, fx, fk = case["fc1_yxk"]
+        w["fc1_w"][(fy * 44 + fx) * 48 + fk, 0] = 1.0
+        w["fc2_w"][0, 0] = 1.0
+        w["cls_w"][0] = [1.0, 0.0, -1.0]
+        w["mic_w"][0] = 1.0
+        s = oracle.classify(img, np.array([case["hit"]]), w)[0]
+        expect = hit_scores if case["hit_expected"] else miss_scores
+        np.testing.assert_allclose(s, expect, rtol=1e-7, atol=0, err_msg=str(case))
+
+
+def test_full_network_matches_torch_fp64():
+    w = synth.he_normal_weights()
+    P = synth.config4_patches(6, seed=77)
+    got = oracle.forward(P, w)
+    d = {k: torch.from_numpy(v).double() for k, v in w.items()}
+    x = torch.from_numpy(P).double()[:, None]
+    A = torch.relu(torch.nn.functional.conv2d(x, d["conv_w"][:, None], d["conv_b"]))
+    a = A.permute(0, 2, 3, 1).reshape(6, -1)
+    h1 = torch.relu(torch.nn.functional.linear(a, d["fc1_w"].T, d["fc1_b"]))
+    h2 = torch.relu(torch.nn.functional.linear(h1, d["fc2_w"].T, d["fc2_b"]))
+    s = torch.softmax(torch.nn.functional.linear(h2, d["cls_w"].T, d["cls_b"]), dim=1)
+    m = torch.sigmoid(h2 @ d["mic_w"] + d["mic_b"])
+    ref = torch.cat([s, m[:, None]], 1).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-13)
+
+
+def test_scores_fp32_softmax_sum():
+    p = synth.config1()
+    w = synth.he_normal_weights()
+    s = oracle.classify(p.image, p.hits[:64], w)
+    assert s.dtype == np.float32 and s.shape == (64, 4)
+    assert np.all(np.abs(s[:, :3].astype(np.float64).sum(1) - 1) <= 2 ** -22)
+    assert np.all((s[:, 3] >= 0) & (s[:, 3] <= 1))
+
+
+# ---------------------------------------------------------------- invariances
+
+def test_permutation_duplicate_and_chunk_invariance():
+    p = synth.config1()
+    w = synth.he_normal_weights()
+    hits = p.hits[:40]
+    base = oracle.classify(p.image, hits, w)
+    perm = np.random.default_rng(8).permutation(len(hits))
+    assert np.array_equal(oracle.classify(p.image, hits[perm], w), base[perm])
+    dup = np.concatenate([hits[:5], hits[:5]])
+    sd = oracle.classify(p.image, dup, w)
+    assert np.array_equal(sd[:5], sd[5:]) and np.array_equal(sd[:5], base[:5])
+    assert np.array_equal(oracle.classify(p.image, hits, w, chunk=7), base)
+
+
+def test_planes_match_single_plane():
+    a = synth.gen_plane(64, 300, 3, 1, 20, seed=11)
+    b = synth.gen_plane(90, 200, 3, 1, 20, seed=12)
+    w = synth.he_normal_weights()
+    h3 = np.concatenate([np.c_[np.ones(len(b.hits), np.int32), b.hits],
+                         np.c_[np.zeros(len(a.hits), np.int32), a.hits]])
+    s = oracle.classify_planes([a.image, b.image], h3, w)
+    assert np.array_equal(s[:len(b.hits)], oracle.classify(b.image, b.hits, w))
+    assert np.array_equal(s[len(b.hits):], oracle.classify(a.image, a.hits, w))
+
+
+def test_bf16_emulation_close_to_full_precision():
+    """The diagnostic bf16-rounded network stays within the bf16 budget of the
+    full-precision oracle on these inputs (sanity of the diagnostic only)."""
+    w = synth.he_normal_weights()
+    P = synth.config4_patches(32, seed=9)
+    full = oracle.forward(P, w)
+    emu = oracle.forward_bf16_emulated(P, w)
+    assert np.max(np.abs(full - emu)) < 2e-2
