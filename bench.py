@@ -1,0 +1,283 @@
+"""Benchmark: hit patches classified per second on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--precision fp32|bf16]
+
+One step is one pass of the whole hot path — patch gather, conv, FC1, FC2 and
+the heads — over one batch of synthetic input already resident in HBM:
+
+* config 3 (default): an event of 18 planes (6 x (800, 800, 480) wires x 6000
+  ticks, fp32 ADC) and 50,000 hits, classified by one pointid_classify_planes
+  call;
+* config 2: one 480 x 6000 plane and 3,000 hits (pointid_classify);
+* config 4: a batch of pre-cut patches (pointid_classify_patches, --batch).
+
+Prints one JSON line on stdout.  `roofline` describes the kernel that takes the
+most time, timed with HIP events on its own stream inside the timed region;
+`cpu_baseline` times the fp64 CPU oracle on a bounded sample of the same
+workload on this host's cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "hit patches classified/sec on 1 MI355X; % MFMA peak (dense+conv)"
+# Per-patch work of the network (paper §2.2).
+CONV_MAC = 44 * 44 * 48 * 25            # 2,323,200
+FC1_MAC = 92928 * 128                   # 11,894,784
+TAIL_MAC = 128 * 32 + 32 * 4            # 4,224
+# MI355X published peaks.
+PEAK = {"mfma_bf16": 2500.0, "mfma_fp32": 157.3, "alu_fp32": 157.3, "hbm": 8000.0}  # TFLOP/s, GB/s
+
+# Kernel name -> (model, source file).  Model gives algorithmic work per patch.
+KERNELS = {
+    "gather": ("bytes", "gather.hip"),
+    "conv_fp32": ("flops_conv", "fp32_vector.hip"),
+    "fc1_fp32": ("flops_fc1", "fp32_vector.hip"),
+    "tail": ("bytes_tail", "tail.hip"),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4])
+    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
+    return ap.parse_args()
+
+
+def source_sha(fname):
+    p = os.path.join(ROOT, "paper_2009_04509_amd", "csrc", fname)
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(kernel, workload_tag):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_tag}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != source_sha(KERNELS[kernel][1]):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def make_workload(args, torch, pid):
+    import synth
+    dev = "cuda:0"
+    if args.config == 3:
+        planes, h3 = synth.config3()
+        imgs = [torch.from_numpy(p.image).to(dev) for p in planes]
+        hits = torch.from_numpy(h3).to(dev)
+        n = len(h3)
+        scores = torch.empty((n, 4), dtype=torch.float32, device=dev)
+        footprint = _footprint([p.image.shape for p in planes], h3)
+
+        def step(h):
+            pid.pointid_classify_planes(h, imgs, hits, scores)
+
+        desc = {"workload": "event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
+                            "50,000 hits, one pointid_classify_planes call",
+                "hits": n, "planes": 18, "ticks": 6000}
+        sample = dict(kind="planes", images=[p.image for p in planes], hits=h3)
+        hit_bytes = 12
+    elif args.config == 2:
+        p = synth.config2()
+        img = torch.from_numpy(p.image).to(dev)
+        hits = torch.from_numpy(p.hits).to(dev)
+        n = len(p.hits)
+        scores = torch.empty((n, 4), dtype=torch.float32, device=dev)
+        h3 = np.c_[np.zeros(n, np.int32), p.hits]
+        footprint = _footprint([p.image.shape], h3)
+
+        def step(h):
+            pid.pointid_classify(h, img, hits, scores)
+
+        desc = {"workload": "plane: 480 wires x 6000 ticks fp32 ADC, 3,000 hits, one "
+                            "pointid_classify call", "hits": n, "planes": 1, "ticks": 6000}
+        sample = dict(kind="plane", image=p.image, hits=p.hits)
+        hit_bytes = 8
+    else:
+        P = synth.config4_patches(args.batch)
+        patches = torch.from_numpy(P).to(dev)
+        n = args.batch
+        scores = torch.empty((n, 4), dtype=torch.float32, device=dev)
+        footprint = 0
+
+        def step(h):
+            pid.pointid_classify_patches(h, patches, scores)
+
+        desc = {"workload": f"pre-cut patch batch of {n} (N(0,1) + one line each), one "
+                            "pointid_classify_patches call", "hits": n}
+        sample = dict(kind="patches", patches=P)
+        hit_bytes = 0
+    return step, n, desc, sample, footprint, hit_bytes
+
+
+def _footprint(shapes, h3):
+    """Distinct image pixels the hits' 48x48 windows touch (the gather's minimal read)."""
+    total = 0
+    for p, (W, T) in enumerate(shapes):
+        sel = h3[h3[:, 0] == p]
+        if not len(sel):
+            continue
+        mask = np.zeros((W + 48, T + 48), np.int8)
+        for w, t in sel[:, 1:]:
+            mask[w:w + 48, t:t + 48] = 1            # offset by 24 on both axes
+        total += int(mask[24:24 + W, 24:24 + T].sum())
+    return total
+
+
+def cpu_baseline(sample, n_sample):
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    w = synth.he_normal_weights()
+    rng = np.random.default_rng(2024)
+    if sample["kind"] == "planes":
+        idx = np.sort(rng.choice(len(sample["hits"]), n_sample, replace=False))
+        t0 = time.perf_counter()
+        oracle.classify_planes(sample["images"], sample["hits"][idx], w)
+        what = f"{n_sample} hits sampled (seeded) from the 50,000-hit event, oracle.classify_planes"
+    elif sample["kind"] == "plane":
+        idx = np.sort(rng.choice(len(sample["hits"]), min(n_sample, len(sample["hits"])), replace=False))
+        t0 = time.perf_counter()
+        oracle.classify(sample["image"], sample["hits"][idx], w)
+        what = f"{len(idx)} hits sampled (seeded) from the plane, oracle.classify"
+    else:
+        idx = np.arange(min(n_sample, len(sample["patches"])))
+        t0 = time.perf_counter()
+        oracle.classify_patches(sample["patches"][idx], w)
+        what = f"first {len(idx)} patches of the batch, oracle.classify_patches"
+    dt = time.perf_counter() - t0
+    return {"value": len(idx) / dt, "unit": "patches/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{what}; {dt:.1f} s", "seconds": round(dt, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); "
+              "the per-hit path shards by hits with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2009_04509_amd import binding as pid
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    log(f"[bench] building config {args.config} workload")
+    step, n, desc, sample, footprint, hit_bytes = make_workload(args, torch, pid)
+    h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step(h)
+    torch.cuda.synchronize()
+
+    pid.pointid_timing_reset()
+    pid.pointid_timing_enable(True)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        step(h)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    pid.pointid_timing_enable(False)
+    ms = ev0.elapsed_time(ev1)
+    ms_step = ms / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})")
+
+    patch_bytes = 9216 if args.precision == "fp32" else 4608
+    kern = {}
+    for name, (model, _src) in KERNELS.items():
+        tot, cnt = pid.pointid_timing_query(name)
+        if cnt == 0:
+            continue
+        per_step_patches = n
+        if model == "bytes":
+            work = args.steps * (per_step_patches * (patch_bytes + hit_bytes) + footprint * 4)
+            unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
+        elif model == "bytes_tail":
+            work = args.steps * per_step_patches * (8 * 128 * 4 + 16)
+            unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
+        else:
+            mac = CONV_MAC if model == "flops_conv" else FC1_MAC
+            work = args.steps * per_step_patches * 2 * mac
+            unit, rate = "TFLOP/s", work / (tot * 1e-3) / 1e12
+        kern[name] = {"ms_per_step": tot / args.steps, "launches": cnt,
+                      "avg_launch_ms": tot / cnt, "achieved": rate, "unit": unit,
+                      "work_per_launch": work / cnt}
+        log(f"[bench] {name:10s} {tot / args.steps:8.3f} ms/step  {cnt} launches  {rate:9.2f} {unit}")
+
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    d = kern[dom]
+    model = KERNELS[dom][0]
+    if model.startswith("flops"):
+        bound, peak = "alu", PEAK["alu_fp32"]
+    else:
+        bound, peak = "hbm", PEAK["hbm"]
+    tag = f"config{args.config}_{args.precision}"
+    traffic = load_traffic(dom, tag)
+    roof = {"kernel": dom, "bound": bound, "achieved": round(d["achieved"], 3), "peak": peak,
+            "unit": d["unit"], "frac": round(d["achieved"] / peak, 4),
+            "traffic": traffic, "avg_launch_ms": round(d["avg_launch_ms"], 4),
+            "work_per_launch": d["work_per_launch"]}
+
+    value = n / (ms_step * 1e-3)
+    total_flop = n * 2 * (CONV_MAC + FC1_MAC + TAIL_MAC)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": args.precision, "data": "synthetic",
+        "config": {**desc, "precision": args.precision},
+        "roofline": roof,
+        "network_tflops": round(total_flop / (ms_step * 1e-3) / 1e12, 3),
+        "kernels": {k: {"ms_per_step": round(v["ms_per_step"], 4), "launches": v["launches"],
+                        "achieved": round(v["achieved"], 3), "unit": v["unit"]}
+                    for k, v in kern.items()},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(sample, args.cpu_sample)
+    h.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

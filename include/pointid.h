@@ -1,0 +1,209 @@
+/*
+ * pointid.h — C ABI of libpointid: per-hit track / shower / Michel
+ * classification on one AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper §2.1 and §2.3): for every reconstructed wire hit, given
+ * by its wire number and peak time, a 48x48 patch is cut from the plane's
+ * deconvolved charge image, rows indexing the wire and columns the time, and
+ * classified by the CNN of paper §2.2 — 48 filters of 5x5 at stride 1 (48 maps
+ * of 44x44) with ReLU, a 128-neuron and a 32-neuron fully connected layer with
+ * ReLU, then a 3-output softmax branch and a 1-output sigmoid (Michel) branch.
+ *
+ * Readings of the paper fixed by this ABI:
+ *   - patch pixel (r, c) of hit (w, t) is image[w - 24 + r][t - 24 + c]; any
+ *     pixel outside the plane reads 0 (so the hit sits at pixel (24, 24));
+ *   - one image column is one time tick; the image is not rescaled;
+ *   - the filter is a cross-correlation (no flip); the maps are flattened
+ *     channels-last, FC1 input index (y*44 + x)*48 + k;
+ *   - dropout is the identity at inference.
+ *
+ * Conventions for every entry point:
+ *   - All pointers named image/hits/patches/scores are DEVICE pointers on the
+ *     handle's device, owned by the caller, who keeps them alive until the
+ *     stream has passed the call.  Weight pointers are HOST pointers.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
+ *     only enqueue work on it; none synchronises the host.  Temporary device
+ *     memory is taken from the device's stream-ordered pool on `stream` and
+ *     returned to it on `stream`.
+ *   - A handle is immutable after pointid_create: any number of host threads
+ *     and streams may use one handle at once.
+ *   - Results are deterministic: identical inputs give identical bits, and
+ *     permuting the hits permutes the scores bit for bit (no atomics, fixed
+ *     reduction order).
+ *   - Status codes are returned; arguments are validated on the host before any
+ *     launch; no C++ exception crosses the ABI.  On a non-OK status,
+ *     pointid_last_error() returns a description for the calling thread.
+ *   - n == 0 is a successful no-op (no launch, pointers may be NULL).
+ *   - Hit coordinates are never errors: pixels outside their plane read 0,
+ *     whole patches included; a plane index out of range gives an all-zero
+ *     patch.  Inputs must be finite (not checked).
+ */
+#ifndef POINTID_H
+#define POINTID_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+enum {
+    POINTID_OK = 0,
+    POINTID_EINVAL = -1,        /* bad argument (NULL pointer, negative size, ...) */
+    POINTID_ENOMEM = -2,        /* device allocation failed */
+    POINTID_EHIP = -3,          /* a HIP runtime call or kernel launch failed */
+    POINTID_ENODEV = -4,        /* no usable gfx950 device */
+    POINTID_EUNSUPPORTED = -5   /* precision or dtype not supported */
+};
+
+/* arithmetic of a handle (pointid_create) or element type of a patch buffer */
+enum {
+    POINTID_FP32 = 0,           /* fp32 inputs, weights, accumulation */
+    POINTID_BF16 = 1            /* bf16 patch, conv filter, conv output and FC1
+                                   filter (round to nearest even); fp32
+                                   accumulation, biases, FC2 and heads */
+};
+
+/* Patch and network shape, paper §2.1-§2.2. */
+#define POINTID_PATCH 48
+#define POINTID_KSIZE 5
+#define POINTID_NCH 48
+#define POINTID_FMAP 44
+#define POINTID_FC1_IN 92928     /* 44 * 44 * 48 */
+#define POINTID_FC1_OUT 128
+#define POINTID_FC2_OUT 32
+#define POINTID_NCLS 3
+#define POINTID_NSCORES 4        /* (p_track, p_em, p_none, p_michel) */
+#define POINTID_MAX_PLANES 64
+
+typedef struct pointid_s *pointid_handle;
+
+/*
+ * Host fp32 weights of the network of paper §2.2 (11,900,420 values), all
+ * C-contiguous, owned by the caller and only read during pointid_create.
+ */
+typedef struct {
+    const float *conv_w;   /* [48][5][5]: filter k, u = wire offset, v = tick offset */
+    const float *conv_b;   /* [48] */
+    const float *fc1_w;    /* [92928][128]: row (y*44 + x)*48 + k */
+    const float *fc1_b;    /* [128] */
+    const float *fc2_w;    /* [128][32] */
+    const float *fc2_b;    /* [32] */
+    const float *cls_w;    /* [32][3]  softmax branch */
+    const float *cls_b;    /* [3] */
+    const float *mic_w;    /* [32]     sigmoid (Michel) branch */
+    const float *mic_b;    /* [1] */
+} pointid_weights;
+
+/* One plane of a multi-plane call: device fp32 image [n_wires][n_ticks],
+ * tick fastest (row pitch n_ticks floats). */
+typedef struct {
+    const float *image;
+    int32_t n_wires;
+    int32_t n_ticks;
+} pointid_plane;
+
+/*
+ * Create a classifier on `device` (HIP ordinal) computing in `precision`
+ * (POINTID_FP32 or POINTID_BF16).  The weights are converted and repacked into
+ * device memory owned by the handle; the call is synchronous, so the host
+ * weights may be freed when it returns.
+ * Errors: EINVAL (NULL w, NULL member, NULL out), EUNSUPPORTED (precision),
+ * ENODEV (no such device, or not gfx950), ENOMEM, EHIP.  *out is set to NULL
+ * on failure.
+ */
+int pointid_create(const pointid_weights *w, int precision, int device,
+                   pointid_handle *out);
+
+/* Free a handle (synchronises its device first).  NULL is a no-op. */
+int pointid_destroy(pointid_handle h);
+
+/* Precision the handle was created with, or EINVAL for NULL. */
+int pointid_precision(pointid_handle h);
+
+/*
+ * Classify hits of one plane (paper §2.3: the module passes each hit's wire
+ * number and peak time; the patch is built and classified).
+ *   image  device fp32 [n_wires][n_ticks]
+ *   hits   device int32 [n_hits][2] = (wire, tick)
+ *   scores device fp32 [n_hits][4] = (p_track, p_em, p_none, p_michel), written
+ *          in hit order; the first three sum to 1 (softmax), the last is the
+ *          sigmoid output.  16-byte aligned.
+ * Errors: EINVAL (NULL handle; n_hits < 0; n_wires or n_ticks <= 0; NULL
+ * pointer with n_hits > 0; misaligned scores), ENOMEM (workspace), EHIP
+ * (launch).
+ */
+int pointid_classify(pointid_handle h, const float *image, int32_t n_wires,
+                     int32_t n_ticks, const int32_t *hits, int64_t n_hits,
+                     float *scores, void *stream);
+
+/*
+ * Classify hits spread over several planes in one call (an event, paper §2.1:
+ * data are processed per wire plane).
+ *   planes  HOST array of n_planes descriptors (1 <= n_planes <= 64), read
+ *           during the call only
+ *   hits    device int32 [n_hits][3] = (plane, wire, tick)
+ *   scores  device fp32 [n_hits][4], in hit order
+ * Errors as pointid_classify, plus EINVAL for n_planes out of range or a plane
+ * with a NULL image or non-positive size.
+ */
+int pointid_classify_planes(pointid_handle h, const pointid_plane *planes,
+                            int32_t n_planes, const int32_t *hits,
+                            int64_t n_hits, float *scores, void *stream);
+
+/*
+ * Classify pre-cut patches (the model interface of paper §2.3, which receives
+ * batches of ready patches).
+ *   patches device fp32 [n][48][48] (row = wire, column = tick), 16-byte aligned
+ *   scores  device fp32 [n][4], 16-byte aligned
+ * Errors: EINVAL (NULL handle, n < 0, NULL or misaligned pointer with n > 0),
+ * ENOMEM, EHIP.
+ */
+int pointid_classify_patches(pointid_handle h, const float *patches, int64_t n,
+                             float *scores, void *stream);
+
+/*
+ * Patch construction alone (paper §2.1), for checking and preprocessing; needs
+ * no handle and runs on the current HIP device.
+ *   patches_out device [n_hits][48][48] of fp32 (out_dtype POINTID_FP32) or
+ *               bf16 bit patterns (POINTID_BF16, round to nearest even),
+ *               16-byte aligned; the image may have any alignment
+ * Bit-exact: fp32 values are copied, never computed.
+ * Errors: EINVAL, EUNSUPPORTED (out_dtype), EHIP.
+ */
+int pointid_gather(const float *image, int32_t n_wires, int32_t n_ticks,
+                   const int32_t *hits, int64_t n_hits, void *patches_out,
+                   int out_dtype, void *stream);
+
+/* Multi-plane patch construction; hits are (plane, wire, tick) as in
+ * pointid_classify_planes. */
+int pointid_gather_planes(const pointid_plane *planes, int32_t n_planes,
+                          const int32_t *hits, int64_t n_hits,
+                          void *patches_out, int out_dtype, void *stream);
+
+/*
+ * Kernel timing for measurement tools (not needed for classification).  While
+ * enabled (process-wide), every kernel this library launches is bracketed by
+ * two HIP events recorded on the stream the kernel runs on.
+ * pointid_timing_query waits for the recorded events of the kernel named
+ * `kernel` ("gather", "conv_fp32", "fc1_fp32", "tail", ...) and returns the
+ * summed elapsed milliseconds and the number of launches since the last
+ * pointid_timing_reset.  Unknown names return 0 launches.
+ * Errors: EINVAL (NULL output pointer), EHIP (event failure).
+ */
+int pointid_timing_enable(int on);
+int pointid_timing_reset(void);
+int pointid_timing_query(const char *kernel, double *total_ms, int64_t *launches);
+
+/* Text of the last non-OK status on the calling thread ("" if none). */
+const char *pointid_last_error(void);
+
+/* Library version string. */
+const char *pointid_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POINTID_H */

@@ -1,0 +1,281 @@
+"""ctypes binding of libpointid (include/pointid.h), argument marshalling only.
+
+Each function carries the name of the C entry point it calls.  Tensors are
+torch tensors on the handle's device; the binding checks dtype, shape and
+contiguity, passes raw device pointers and the current HIP stream, and raises
+``PointIdError`` on a non-OK status.  Every step of the computation runs in the
+library's HIP kernels; if the library is not built this module fails to import.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpointid.so")
+
+POINTID_OK = 0
+POINTID_EINVAL = -1
+POINTID_ENOMEM = -2
+POINTID_EHIP = -3
+POINTID_ENODEV = -4
+POINTID_EUNSUPPORTED = -5
+POINTID_FP32 = 0
+POINTID_BF16 = 1
+MAX_PLANES = 64
+
+_STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ENODEV", -5: "EUNSUPPORTED"}
+_WEIGHT_FIELDS = ("conv_w", "conv_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b",
+                  "cls_w", "cls_b", "mic_w", "mic_b")
+_WEIGHT_SIZES = {"conv_w": 48 * 25, "conv_b": 48, "fc1_w": 92928 * 128, "fc1_b": 128,
+                 "fc2_w": 128 * 32, "fc2_b": 32, "cls_w": 32 * 3, "cls_b": 3,
+                 "mic_w": 32, "mic_b": 1}
+
+
+class PointIdError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class _Weights(ctypes.Structure):
+    _fields_ = [(name, ctypes.POINTER(ctypes.c_float)) for name in _WEIGHT_FIELDS]
+
+
+class _Plane(ctypes.Structure):
+    _fields_ = [("image", ctypes.c_void_p), ("n_wires", ctypes.c_int32),
+                ("n_ticks", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2009_04509_amd.build` "
+            "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, cint = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int
+    sig = {
+        "pointid_create": (cint, [ctypes.POINTER(_Weights), cint, cint, ctypes.POINTER(vp)]),
+        "pointid_destroy": (cint, [vp]),
+        "pointid_precision": (cint, [vp]),
+        "pointid_classify": (cint, [vp, vp, i32, i32, vp, i64, vp, vp]),
+        "pointid_classify_planes": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp, vp]),
+        "pointid_classify_patches": (cint, [vp, vp, i64, vp, vp]),
+        "pointid_gather": (cint, [vp, i32, i32, vp, i64, vp, cint, vp]),
+        "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
+        "pointid_timing_enable": (cint, [cint]),
+        "pointid_timing_reset": (cint, []),
+        "pointid_timing_query": (cint, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64)]),
+        "pointid_last_error": (ctypes.c_char_p, []),
+        "pointid_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_classify",
+            "pointid_classify_planes", "pointid_classify_patches", "pointid_gather",
+            "pointid_gather_planes", "pointid_timing_enable", "pointid_timing_reset",
+            "pointid_timing_query", "pointid_last_error", "pointid_version")
+
+
+def _check(status: int):
+    if status != POINTID_OK:
+        raise PointIdError(status, lib.pointid_last_error().decode())
+    return status
+
+
+def pointid_last_error() -> str:
+    return lib.pointid_last_error().decode()
+
+
+def pointid_version() -> str:
+    return lib.pointid_version().decode()
+
+
+def pointid_timing_enable(on: bool = True):
+    _check(lib.pointid_timing_enable(1 if on else 0))
+
+
+def pointid_timing_reset():
+    _check(lib.pointid_timing_reset())
+
+
+def pointid_timing_query(kernel: str):
+    """(total_ms, launches) of `kernel` since the last reset."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(lib.pointid_timing_query(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def _precision(p) -> int:
+    if isinstance(p, str):
+        return {"fp32": POINTID_FP32, "bf16": POINTID_BF16}[p]
+    return int(p)
+
+
+def _stream_ptr(stream, device=None):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _need(t, dtype, name, device=None, tail_shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{name} is on cuda:{t.device.index}, handle is on cuda:{device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if tail_shape is not None and tuple(t.shape[1:]) != tuple(tail_shape):
+        raise ValueError(f"{name} must have shape [n, {', '.join(map(str, tail_shape))}]")
+
+
+class Handle:
+    """A created classifier; frees itself on garbage collection."""
+
+    def __init__(self, raw: ctypes.c_void_p, device: int, precision: int):
+        self._raw = raw
+        self.device = device
+        self.precision = precision
+
+    @property
+    def raw(self):
+        if not self._raw:
+            raise ValueError("handle was destroyed")
+        return self._raw
+
+    def close(self):
+        if self._raw:
+            _check(lib.pointid_destroy(self._raw))
+            self._raw = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def pointid_create(weights: dict, precision="fp32", device: int = 0) -> Handle:
+    """Upload ``weights`` (dict of float32 arrays, layouts of include/pointid.h)."""
+    arrays = {}
+    for name in _WEIGHT_FIELDS:
+        a = np.ascontiguousarray(np.asarray(weights[name], dtype=np.float32))
+        if a.size != _WEIGHT_SIZES[name]:
+            raise ValueError(f"{name} has {a.size} values, expected {_WEIGHT_SIZES[name]}")
+        arrays[name] = a
+    w = _Weights(**{n: arrays[n].ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+                    for n in _WEIGHT_FIELDS})
+    raw = ctypes.c_void_p()
+    prec = _precision(precision)
+    _check(lib.pointid_create(ctypes.byref(w), prec, int(device), ctypes.byref(raw)))
+    return Handle(raw, int(device), prec)
+
+
+def pointid_destroy(h: Handle):
+    h.close()
+
+
+def pointid_classify(h: Handle, image: torch.Tensor, hits: torch.Tensor,
+                     scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Scores [n][4] for int32 hits [n][2] = (wire, tick) on fp32 image [W][T]."""
+    _need(image, torch.float32, "image", h.device)
+    if image.dim() != 2:
+        raise ValueError("image must be [n_wires][n_ticks]")
+    _need(hits, torch.int32, "hits", h.device, (2,))
+    n = hits.shape[0]
+    if scores is None:
+        scores = torch.empty((n, 4), dtype=torch.float32, device=image.device)
+    _need(scores, torch.float32, "scores", h.device, (4,))
+    _check(lib.pointid_classify(h.raw, _ptr(image), image.shape[0], image.shape[1], _ptr(hits),
+                                n, _ptr(scores), _stream_ptr(stream, image.device)))
+    return scores
+
+
+def _plane_array(images):
+    if len(images) < 1 or len(images) > MAX_PLANES:
+        raise ValueError("between 1 and 64 planes")
+    arr = (_Plane * len(images))()
+    for i, im in enumerate(images):
+        _need(im, torch.float32, f"images[{i}]")
+        if im.dim() != 2:
+            raise ValueError("each image must be [n_wires][n_ticks]")
+        arr[i] = _Plane(im.data_ptr(), im.shape[0], im.shape[1])
+    return arr
+
+
+def pointid_classify_planes(h: Handle, images, hits: torch.Tensor,
+                            scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Scores for int32 hits [n][3] = (plane, wire, tick) over a list of plane images."""
+    arr = _plane_array(images)
+    _need(hits, torch.int32, "hits", h.device, (3,))
+    n = hits.shape[0]
+    if scores is None:
+        scores = torch.empty((n, 4), dtype=torch.float32, device=hits.device)
+    _need(scores, torch.float32, "scores", h.device, (4,))
+    _check(lib.pointid_classify_planes(h.raw, arr, len(images), _ptr(hits), n, _ptr(scores),
+                                       _stream_ptr(stream, hits.device)))
+    return scores
+
+
+def pointid_classify_patches(h: Handle, patches: torch.Tensor,
+                             scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Scores for fp32 patches [n][48][48]."""
+    _need(patches, torch.float32, "patches", h.device, (48, 48))
+    n = patches.shape[0]
+    if scores is None:
+        scores = torch.empty((n, 4), dtype=torch.float32, device=patches.device)
+    _need(scores, torch.float32, "scores", h.device, (4,))
+    _check(lib.pointid_classify_patches(h.raw, _ptr(patches), n, _ptr(scores),
+                                        _stream_ptr(stream, patches.device)))
+    return scores
+
+
+def pointid_gather(image: torch.Tensor, hits: torch.Tensor, out_dtype="fp32",
+                   out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Patches [n][48][48]: float32, or bf16 bit patterns as int16 for ``out_dtype='bf16'``."""
+    _need(image, torch.float32, "image")
+    _need(hits, torch.int32, "hits", None, (2,))
+    code = _precision(out_dtype)
+    n = hits.shape[0]
+    tdt = torch.float32 if code == POINTID_FP32 else torch.int16
+    if out is None:
+        out = torch.empty((n, 48, 48), dtype=tdt, device=image.device)
+    _check(lib.pointid_gather(_ptr(image), image.shape[0], image.shape[1], _ptr(hits), n,
+                              _ptr(out), code, _stream_ptr(stream, image.device)))
+    return out
+
+
+def pointid_gather_planes(images, hits: torch.Tensor, out_dtype="fp32",
+                          out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    arr = _plane_array(images)
+    _need(hits, torch.int32, "hits", None, (3,))
+    code = _precision(out_dtype)
+    n = hits.shape[0]
+    tdt = torch.float32 if code == POINTID_FP32 else torch.int16
+    if out is None:
+        out = torch.empty((n, 48, 48), dtype=tdt, device=hits.device)
+    _check(lib.pointid_gather_planes(arr, len(images), _ptr(hits), n, _ptr(out), code,
+                                     _stream_ptr(stream, hits.device)))
+    return out

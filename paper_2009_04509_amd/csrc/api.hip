@@ -1,0 +1,416 @@
+// C ABI of libpointid (declared in include/pointid.h): argument validation,
+// weight upload, workspace from the stream-ordered pool, launch sequencing.
+// Every call only enqueues work on the caller's stream.
+#include "pointid.h"
+
+#include <atomic>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace pointid;
+
+struct pointid_s {
+  int device;
+  int precision;
+  DeviceWeights w;     // device pointers into `blob`
+  void* blob;          // one allocation holding every parameter tensor
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) ? POINTID_ENOMEM
+                                                                      : POINTID_EHIP;
+}
+
+// Makes `dev` current for the scope of a call and restores the caller's device.
+class DeviceScope {
+ public:
+  explicit DeviceScope(int dev) {
+    if (hipGetDevice(&old_) != hipSuccess) old_ = -1;
+    if (old_ != dev) err_ = hipSetDevice(dev);
+  }
+  ~DeviceScope() {
+    if (old_ >= 0 && err_ == hipSuccess) (void)hipSetDevice(old_);
+  }
+  hipError_t error() const { return err_; }
+
+ private:
+  int old_ = -1;
+  hipError_t err_ = hipSuccess;
+};
+
+// ---- optional per-kernel timing (pointid_timing_*)
+struct TimingRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+struct Timing {
+  std::atomic<bool> on{false};
+  std::mutex mu;
+  std::vector<TimingRec> pending;
+  std::map<std::string, std::pair<double, int64_t>> total;
+};
+Timing& timing() {
+  static Timing t;
+  return t;
+}
+
+// Brackets one launch with events on its stream while timing is enabled.
+class KernelTimer {
+ public:
+  KernelTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
+    if (!timing().on.load(std::memory_order_relaxed)) return;
+    if (hipEventCreate(&a_) != hipSuccess) return;
+    if (hipEventRecord(a_, s_) != hipSuccess) {
+      (void)hipEventDestroy(a_);
+      return;
+    }
+    active_ = true;
+  }
+  ~KernelTimer() {
+    if (!active_) return;
+    hipEvent_t b;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a_);
+      return;
+    }
+    (void)hipEventRecord(b, s_);
+    std::lock_guard<std::mutex> g(timing().mu);
+    timing().pending.push_back({name_, a_, b});
+  }
+
+ private:
+  const char* name_;
+  hipStream_t s_;
+  hipEvent_t a_{};
+  bool active_ = false;
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Stream-ordered scratch: allocated on `stream`, freed on `stream` when the
+// scope ends (after the work enqueued in between).
+class Workspace {
+ public:
+  explicit Workspace(hipStream_t s) : s_(s) {}
+  ~Workspace() {
+    for (void* p : ptrs_) (void)hipFreeAsync(p, s_);
+  }
+  hipError_t get(size_t bytes, void** out) {
+    *out = nullptr;
+    if (bytes == 0) return hipSuccess;
+    hipError_t e = hipMallocAsync(out, bytes, s_);
+    if (e == hipSuccess) ptrs_.push_back(*out);
+    return e;
+  }
+
+ private:
+  hipStream_t s_;
+  std::vector<void*> ptrs_;
+};
+
+constexpr int kSplitsFp32 = 8;            // FC1 split-K on the vector fp32 path
+constexpr int64_t kChunkFp32 = 2048;      // patches whose maps are live at once
+
+// patches (fp32 [n][2304]) -> scores; the shared back half of every classify.
+int run_network(pointid_handle h, const float* patches, int64_t n, float* scores,
+                hipStream_t stream, Workspace& ws) {
+  const int S = kSplitsFp32;
+  float* part = nullptr;
+  float* act = nullptr;
+  const int64_t chunk = n < kChunkFp32 ? n : kChunkFp32;
+  hipError_t e = ws.get(sizeof(float) * (size_t)S * n * kFc1Out, (void**)&part);
+  if (e != hipSuccess) return hip_fail(e, "workspace (FC1 partials)");
+  e = ws.get(sizeof(float) * (size_t)chunk * kFc1In, (void**)&act);
+  if (e != hipSuccess) return hip_fail(e, "workspace (conv maps)");
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    const int64_t m = (n - c0) < chunk ? (n - c0) : chunk;
+    {
+      KernelTimer kt("conv_fp32", stream);
+      e = launch_conv_fp32(patches + c0 * kPatchPix, m, h->w, act, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "conv launch");
+    {
+      KernelTimer kt("fc1_fp32", stream);
+      e = launch_fc1_fp32(act, m, c0, n, h->w, S, part, stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "fc1 launch");
+  }
+  {
+    KernelTimer kt("tail", stream);
+    e = launch_tail(part, S, n, h->w, scores, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "tail launch");
+  return POINTID_OK;
+}
+
+int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hits,
+                  int stride, int64_t n, float* scores, void* stream_) {
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  Workspace ws(stream);
+  float* patches = nullptr;
+  hipError_t e = ws.get(sizeof(float) * (size_t)n * kPatchPix, (void**)&patches);
+  if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
+  {
+    KernelTimer kt("gather", stream);
+    e = launch_gather(planes, hits, stride, n, patches, false, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return run_network(h, patches, n, scores, stream, ws);
+}
+
+int check_planes(const pointid_plane* planes, int32_t n_planes, PlaneTable* t) {
+  if (!planes) return fail(POINTID_EINVAL, "planes is NULL");
+  if (n_planes < 1 || n_planes > kMaxPlanes)
+    return fail(POINTID_EINVAL, "n_planes must be in [1, 64]");
+  std::memset(t, 0, sizeof(*t));
+  t->n = n_planes;
+  for (int i = 0; i < n_planes; ++i) {
+    if (!planes[i].image) return fail(POINTID_EINVAL, "plane " + std::to_string(i) + " image is NULL");
+    if (planes[i].n_wires <= 0 || planes[i].n_ticks <= 0)
+      return fail(POINTID_EINVAL, "plane " + std::to_string(i) + " has a non-positive size");
+    t->p[i].image = planes[i].image;
+    t->p[i].n_wires = planes[i].n_wires;
+    t->p[i].n_ticks = planes[i].n_ticks;
+  }
+  return POINTID_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pointid_last_error(void) { return g_err.c_str(); }
+
+const char* pointid_version(void) { return "libpointid 0.1 (gfx950)"; }
+
+int pointid_timing_enable(int on) {
+  timing().on.store(on != 0);
+  return POINTID_OK;
+}
+
+int pointid_timing_reset(void) {
+  Timing& T = timing();
+  std::lock_guard<std::mutex> g(T.mu);
+  for (TimingRec& r : T.pending) {
+    (void)hipEventSynchronize(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  T.pending.clear();
+  T.total.clear();
+  return POINTID_OK;
+}
+
+int pointid_timing_query(const char* kernel, double* total_ms, int64_t* launches) {
+  if (!kernel || !total_ms || !launches) return fail(POINTID_EINVAL, "NULL argument");
+  Timing& T = timing();
+  std::lock_guard<std::mutex> g(T.mu);
+  int rc = POINTID_OK;
+  for (TimingRec& r : T.pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) rc = hip_fail(e, "timing event");
+    auto& slot = T.total[r.name];
+    slot.first += ms;
+    slot.second += 1;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  T.pending.clear();
+  auto it = T.total.find(kernel);
+  *total_ms = it == T.total.end() ? 0.0 : it->second.first;
+  *launches = it == T.total.end() ? 0 : it->second.second;
+  return rc;
+}
+
+int pointid_create(const pointid_weights* w, int precision, int device,
+                   pointid_handle* out) {
+  if (!out) return fail(POINTID_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!w) return fail(POINTID_EINVAL, "weights is NULL");
+  const float* members[] = {w->conv_w, w->conv_b, w->fc1_w, w->fc1_b, w->fc2_w,
+                            w->fc2_b,  w->cls_w,  w->cls_b, w->mic_w, w->mic_b};
+  for (const float* m : members)
+    if (!m) return fail(POINTID_EINVAL, "a weight pointer is NULL");
+  if (precision != POINTID_FP32)
+    return fail(POINTID_EUNSUPPORTED, "precision not supported by this build");
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0)
+    return fail(POINTID_ENODEV, "no HIP device visible");
+  if (device < 0 || device >= count)
+    return fail(POINTID_ENODEV, "device ordinal out of range");
+  hipDeviceProp_t prop;
+  hipError_t e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(POINTID_ENODEV, std::string("device is ") + prop.gcnArchName + ", library is built for gfx950");
+  DeviceScope dev(device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+
+  // Keep freed stream-ordered workspace cached in the pool instead of
+  // returning it to the OS after every call.
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
+    uint64_t thr = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  }
+
+  struct Piece { const float* src; size_t count; const float** dst; };
+  auto* hnd = new (std::nothrow) pointid_s();
+  if (!hnd) return fail(POINTID_ENOMEM, "host allocation failed");
+  hnd->device = device;
+  hnd->precision = precision;
+  hnd->w.precision = precision;
+  Piece pieces[] = {
+      {w->conv_w, (size_t)kCh * kK * kK, &hnd->w.conv_w},
+      {w->conv_b, (size_t)kCh, &hnd->w.conv_b},
+      {w->fc1_w, (size_t)kFc1In * kFc1Out, &hnd->w.fc1_w},
+      {w->fc1_b, (size_t)kFc1Out, &hnd->w.fc1_b},
+      {w->fc2_w, (size_t)kFc1Out * kFc2Out, &hnd->w.fc2_w},
+      {w->fc2_b, (size_t)kFc2Out, &hnd->w.fc2_b},
+      {w->cls_w, (size_t)kFc2Out * kNcls, &hnd->w.cls_w},
+      {w->cls_b, (size_t)kNcls, &hnd->w.cls_b},
+      {w->mic_w, (size_t)kFc2Out, &hnd->w.mic_w},
+      {w->mic_b, (size_t)1, &hnd->w.mic_b},
+  };
+  size_t total = 0;
+  std::vector<size_t> offs;
+  for (const Piece& p : pieces) {
+    offs.push_back(total);
+    total += (p.count * sizeof(float) + 255) & ~size_t(255);
+  }
+  e = hipMalloc(&hnd->blob, total);
+  if (e != hipSuccess) {
+    delete hnd;
+    return hip_fail(e, "hipMalloc(weights)");
+  }
+  for (size_t i = 0; i < sizeof(pieces) / sizeof(pieces[0]); ++i) {
+    char* d = static_cast<char*>(hnd->blob) + offs[i];
+    e = hipMemcpy(d, pieces[i].src, pieces[i].count * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(hnd->blob);
+      delete hnd;
+      return hip_fail(e, "hipMemcpy(weights)");
+    }
+    *pieces[i].dst = reinterpret_cast<const float*>(d);
+  }
+  *out = hnd;
+  return POINTID_OK;
+}
+
+int pointid_destroy(pointid_handle h) {
+  if (!h) return POINTID_OK;
+  {
+    DeviceScope dev(h->device);
+    (void)hipDeviceSynchronize();
+    if (h->blob) (void)hipFree(h->blob);
+  }
+  delete h;
+  return POINTID_OK;
+}
+
+int pointid_precision(pointid_handle h) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  return h->precision;
+}
+
+int pointid_classify(pointid_handle h, const float* image, int32_t n_wires,
+                     int32_t n_ticks, const int32_t* hits, int64_t n_hits,
+                     float* scores, void* stream) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  if (n_wires <= 0 || n_ticks <= 0) return fail(POINTID_EINVAL, "n_wires and n_ticks must be positive");
+  if (n_hits == 0) return POINTID_OK;
+  if (!image || !hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
+  PlaneTable t;
+  std::memset(&t, 0, sizeof(t));
+  t.n = 1;
+  t.p[0] = {image, n_wires, n_ticks};
+  return classify_hits(h, t, hits, 2, n_hits, scores, stream);
+}
+
+int pointid_classify_planes(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
+                            const int32_t* hits, int64_t n_hits, float* scores,
+                            void* stream) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (n_hits == 0) return POINTID_OK;
+  if (!hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
+  return classify_hits(h, t, hits, 3, n_hits, scores, stream);
+}
+
+int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
+                             float* scores, void* stream_) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n < 0) return fail(POINTID_EINVAL, "n is negative");
+  if (n == 0) return POINTID_OK;
+  if (!patches || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(scores) || !aligned16(patches))
+    return fail(POINTID_EINVAL, "patches and scores must be 16-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  Workspace ws(stream);
+  return run_network(h, patches, n, scores, stream, ws);
+}
+
+int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,
+                   const int32_t* hits, int64_t n_hits, void* patches_out,
+                   int out_dtype, void* stream) {
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  if (n_wires <= 0 || n_ticks <= 0) return fail(POINTID_EINVAL, "n_wires and n_ticks must be positive");
+  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16)
+    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32 or POINTID_BF16");
+  if (n_hits == 0) return POINTID_OK;
+  if (!image || !hits || !patches_out) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(patches_out)) return fail(POINTID_EINVAL, "patches_out must be 16-byte aligned");
+  PlaneTable t;
+  std::memset(&t, 0, sizeof(t));
+  t.n = 1;
+  t.p[0] = {image, n_wires, n_ticks};
+  hipError_t e = launch_gather(t, hits, 2, n_hits, patches_out, out_dtype == POINTID_BF16,
+                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
+}
+
+int pointid_gather_planes(const pointid_plane* planes, int32_t n_planes, const int32_t* hits,
+                          int64_t n_hits, void* patches_out, int out_dtype, void* stream) {
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16)
+    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32 or POINTID_BF16");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (n_hits == 0) return POINTID_OK;
+  if (!hits || !patches_out) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(patches_out)) return fail(POINTID_EINVAL, "patches_out must be 16-byte aligned");
+  hipError_t e = launch_gather(t, hits, 3, n_hits, patches_out, out_dtype == POINTID_BF16,
+                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
+}
+
+}  // extern "C"

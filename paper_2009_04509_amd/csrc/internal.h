@@ -1,0 +1,75 @@
+// Internal interface between the C-ABI layer (api.hip) and the HIP kernels.
+// Not installed; nothing here is part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace pointid {
+
+constexpr int kPatch = 48;                  // patch side (paper §2.1)
+constexpr int kHalf = 24;                   // hit sits at patch pixel (24, 24)
+constexpr int kK = 5;                       // filter side (paper §2.2)
+constexpr int kCh = 48;                     // filters
+constexpr int kFm = 44;                     // map side = 48 - 5 + 1
+constexpr int kPos = kFm * kFm;             // 1936 map positions
+constexpr int kFc1In = kPos * kCh;          // 92928
+constexpr int kFc1Out = 128;
+constexpr int kFc2Out = 32;
+constexpr int kNcls = 3;
+constexpr int kPatchPix = kPatch * kPatch;  // 2304
+constexpr int kMaxPlanes = 64;
+
+struct PlaneDesc {
+  const float* image;
+  int32_t n_wires;
+  int32_t n_ticks;
+};
+
+// Passed by value as a kernel argument (64 * 16 B + 4 B, inside the 4 KiB limit).
+struct PlaneTable {
+  PlaneDesc p[kMaxPlanes];
+  int32_t n;
+};
+
+// Device-resident parameters of one handle.  fp32 tensors are in the ABI
+// layouts; packed tensors are in the layouts the MFMA kernels read.
+struct DeviceWeights {
+  int precision;             // POINTID_FP32 / POINTID_BF16
+  const float* conv_w;       // [48][25] fp32
+  const float* conv_b;       // [48]
+  const float* fc1_w;        // [92928][128] fp32 (fp32 handles)
+  const float* fc1_b;        // [128]
+  const float* fc2_w;        // [128][32]
+  const float* fc2_b;        // [32]
+  const float* cls_w;        // [32][3]
+  const float* cls_b;        // [3]
+  const float* mic_w;        // [32]
+  const float* mic_b;        // [1]
+};
+
+// Patch construction.  hits: int32 rows of `hit_stride` (2 = (wire, tick) on
+// plane 0, 3 = (plane, wire, tick)).  out: [n][48][48] fp32 or bf16 bits.
+hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
+                         int hit_stride, int64_t n, void* out, bool out_bf16,
+                         hipStream_t stream);
+
+// fp32 conv + ReLU for patches [n][2304] -> activations [n][92928] (HWC).
+hipError_t launch_conv_fp32(const float* patches, int64_t n,
+                            const DeviceWeights& w, float* act,
+                            hipStream_t stream);
+
+// fp32 FC1 partial products: part[s][row0 + i][128] = sum over split s of
+// act[i][k] * fc1_w[k][n], for i < n.  `n_total` is the row count of `part`.
+hipError_t launch_fc1_fp32(const float* act, int64_t n, int64_t row0,
+                           int64_t n_total, const DeviceWeights& w, int splits,
+                           float* part, hipStream_t stream);
+
+// Reduce the split-K partials in fixed order, then bias+ReLU, FC2+ReLU, the
+// softmax and sigmoid heads: scores [n][4].
+hipError_t launch_tail(const float* part, int splits, int64_t n,
+                       const DeviceWeights& w, float* scores,
+                       hipStream_t stream);
+
+}  // namespace pointid

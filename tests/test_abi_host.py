@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+the header declares, and rejects bad arguments before touching a GPU."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pointid.h")
+
+
+@pytest.fixture(scope="module")
+def b():
+    from paper_2009_04509_amd import binding
+    return binding
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pointid_[a-z_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported(b):
+    names = _declared()
+    assert "pointid_create" in names and "pointid_classify" in names
+    assert set(names) == set(b.EXPORTED)
+    for name in names:
+        assert hasattr(b.lib, name), name
+
+
+def test_version_and_empty_error(b):
+    assert "gfx950" in b.pointid_version()
+    assert isinstance(b.pointid_last_error(), str)
+
+
+NULL = ctypes.c_void_p(0)
+FAKE = ctypes.c_void_p(0x1000)      # never dereferenced: every call below fails validation first
+
+
+def test_classify_validation(b):
+    L = b.lib
+    assert L.pointid_classify(NULL, FAKE, 10, 10, FAKE, 5, FAKE, NULL) == b.POINTID_EINVAL
+    assert "handle" in b.pointid_last_error()
+    assert L.pointid_classify_patches(NULL, FAKE, 5, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_planes(NULL, None, 1, FAKE, 5, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_precision(NULL) == b.POINTID_EINVAL
+
+
+def test_gather_validation(b):
+    L = b.lib
+    assert L.pointid_gather(FAKE, 10, 10, FAKE, -1, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather(FAKE, 0, 10, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather(FAKE, 10, -2, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather(FAKE, 10, 10, FAKE, 3, FAKE, 7, NULL) == b.POINTID_EUNSUPPORTED
+    assert L.pointid_gather(NULL, 10, 10, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather(FAKE, 10, 10, FAKE, 3, ctypes.c_void_p(0x1004), 0, NULL) == b.POINTID_EINVAL
+    assert "aligned" in b.pointid_last_error()
+    # n == 0 is a no-op even with NULL pointers
+    assert L.pointid_gather(NULL, 10, 10, NULL, 0, NULL, 0, NULL) == b.POINTID_OK
+
+
+def test_planes_validation(b):
+    L = b.lib
+    P = b._Plane
+    good = (P * 2)(P(0x1000, 10, 10), P(0x2000, 4, 4))
+    assert L.pointid_gather_planes(good, 0, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather_planes(good, 65, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert "n_planes" in b.pointid_last_error()
+    bad = (P * 2)(P(0x1000, 10, 10), P(0, 4, 4))
+    assert L.pointid_gather_planes(bad, 2, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    bad2 = (P * 2)(P(0x1000, 10, 10), P(0x2000, 0, 4))
+    assert L.pointid_gather_planes(bad2, 2, FAKE, 3, FAKE, 0, NULL) == b.POINTID_EINVAL
+    assert L.pointid_gather_planes(good, 2, NULL, 0, NULL, 0, NULL) == b.POINTID_OK
+
+
+def test_create_validation(b):
+    L = b.lib
+    out = ctypes.c_void_p(123)
+    assert L.pointid_create(None, 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert out.value is None
+    assert L.pointid_create(None, 0, 0, None) == b.POINTID_EINVAL
+    arrays = {n: np.zeros(s, np.float32) for n, s in b._WEIGHT_SIZES.items()}
+    fields = {n: arrays[n].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for n in arrays}
+    w = b._Weights(**fields)
+    assert L.pointid_create(ctypes.byref(w), 9, 0, ctypes.byref(out)) == b.POINTID_EUNSUPPORTED
+    w_missing = b._Weights(**{**fields, "fc1_w": ctypes.POINTER(ctypes.c_float)()})
+    assert L.pointid_create(ctypes.byref(w_missing), 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+
+
+def test_create_without_gpu_is_enodev(b):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is visible")
+    import synth
+    with pytest.raises(b.PointIdError) as e:
+        b.pointid_create(synth.he_normal_weights(), "fp32", 0)
+    assert e.value.status == b.POINTID_ENODEV
+
+
+def test_destroy_null_is_noop(b):
+    assert b.lib.pointid_destroy(NULL) == b.POINTID_OK
+
+
+def test_binding_shape_checks(b):
+    import torch
+    with pytest.raises(ValueError):
+        b.pointid_create({**{n: np.zeros(s, np.float32) for n, s in b._WEIGHT_SIZES.items()},
+                          "fc2_b": np.zeros(5, np.float32)})
+    with pytest.raises((TypeError, ValueError)):
+        b.pointid_gather(torch.zeros(4, 4), torch.zeros(3, 2, dtype=torch.int32))
