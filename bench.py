@@ -42,8 +42,10 @@ PEAK = {"mfma_bf16": 2500.0, "mfma_fp32": 157.3, "alu_fp32": 157.3, "hbm": 8000.
 # Kernel name -> (model, source file).  Model gives algorithmic work per patch.
 KERNELS = {
     "gather": ("bytes", "gather.hip"),
+    "patches_to_16": ("bytes_cast", "gather.hip"),
     "conv_fp32": ("flops_conv", "fp32_vector.hip"),
     "fc1_fp32": ("flops_fc1", "fp32_vector.hip"),
+    "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
     "tail": ("bytes_tail", "tail.hip"),
 }
 
@@ -58,7 +60,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4])
-    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
@@ -235,8 +237,12 @@ def main():
         elif model == "bytes_tail":
             work = args.steps * per_step_patches * (8 * 128 * 4 + 16)
             unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
+        elif model == "bytes_cast":
+            work = args.steps * per_step_patches * (9216 + 4608)
+            unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
         else:
-            mac = CONV_MAC if model == "flops_conv" else FC1_MAC
+            mac = {"flops_conv": CONV_MAC, "flops_fc1": FC1_MAC,
+                   "flops_conv_fc1": CONV_MAC + FC1_MAC}[model]
             work = args.steps * per_step_patches * 2 * mac
             unit, rate = "TFLOP/s", work / (tot * 1e-3) / 1e12
         kern[name] = {"ms_per_step": tot / args.steps, "launches": cnt,
@@ -247,7 +253,9 @@ def main():
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     d = kern[dom]
     model = KERNELS[dom][0]
-    if model.startswith("flops"):
+    if model == "flops_conv_fc1":
+        bound, peak = "mfma", PEAK["mfma_bf16"]       # fp16 and bf16 MFMA share one peak
+    elif model.startswith("flops"):
         bound, peak = "alu", PEAK["alu_fp32"]
     else:
         bound, peak = "hbm", PEAK["hbm"]

@@ -60,9 +60,12 @@ enum {
 /* arithmetic of a handle (pointid_create) or element type of a patch buffer */
 enum {
     POINTID_FP32 = 0,           /* fp32 inputs, weights, accumulation */
-    POINTID_BF16 = 1            /* bf16 patch, conv filter, conv output and FC1
+    POINTID_BF16 = 1,           /* bf16 patch, conv filter, conv output and FC1
                                    filter (round to nearest even); fp32
                                    accumulation, biases, FC2 and heads */
+    POINTID_FP16 = 2            /* as POINTID_BF16 with IEEE fp16 operands:
+                                   same MFMA rate, 3 more mantissa bits; a conv
+                                   output above 65504 in magnitude overflows */
 };
 
 /* Patch and network shape, paper §2.1-§2.2. */
@@ -106,7 +109,7 @@ typedef struct {
 
 /*
  * Create a classifier on `device` (HIP ordinal) computing in `precision`
- * (POINTID_FP32 or POINTID_BF16).  The weights are converted and repacked into
+ * (POINTID_FP32, POINTID_BF16 or POINTID_FP16).  The weights are converted and repacked into
  * device memory owned by the handle; the call is synchronous, so the host
  * weights may be freed when it returns.
  * Errors: EINVAL (NULL w, NULL member, NULL out), EUNSUPPORTED (precision),
@@ -167,7 +170,8 @@ int pointid_classify_patches(pointid_handle h, const float *patches, int64_t n,
  * Patch construction alone (paper §2.1), for checking and preprocessing; needs
  * no handle and runs on the current HIP device.
  *   patches_out device [n_hits][48][48] of fp32 (out_dtype POINTID_FP32) or
- *               bf16 bit patterns (POINTID_BF16, round to nearest even),
+ *               bf16 / fp16 bit patterns (POINTID_BF16 / POINTID_FP16, round to
+ *               nearest even),
  *               16-byte aligned; the image may have any alignment
  * Bit-exact: fp32 values are copied, never computed.
  * Errors: EINVAL, EUNSUPPORTED (out_dtype), EHIP.

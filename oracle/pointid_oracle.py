@@ -107,6 +107,22 @@ def bf16_bits(x) -> np.ndarray:
     return (to_bf16_rne(x).view(np.uint32) >> 16).astype(np.uint16)
 
 
+def to_fp16_rne(x) -> np.ndarray:
+    """Round float32 values to IEEE binary16 (nearest, ties to even), returned
+    as float32 holding the fp16 value (numpy's correctly rounded conversion)."""
+    return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float32)
+
+
+def fp16_bits(x) -> np.ndarray:
+    """uint16 bit patterns of ``to_fp16_rne(x)``."""
+    return np.asarray(x, dtype=np.float32).astype(np.float16).view(np.uint16)
+
+
+def round16(x, kind: str) -> np.ndarray:
+    """Round to the 16-bit operand type ``kind`` ('bf16' or 'fp16')."""
+    return to_bf16_rne(x) if kind == "bf16" else to_fp16_rne(x)
+
+
 # --------------------------------------------------------------------------
 # The network (paper §2.2)
 # --------------------------------------------------------------------------
@@ -212,25 +228,38 @@ def classify_planes(images, hits3, weights, chunk: int = CHUNK) -> np.ndarray:
     return out
 
 
-def quantize_bf16_model(weights) -> dict:
-    """Weights as the bf16 path holds them: conv and FC1 filters rounded to
-    bfloat16 (RNE), everything else unchanged.  Diagnostic use only: the
-    bf16 path is graded against the full-precision oracle."""
+def quantize_16bit_model(weights, kind: str = "bf16") -> dict:
+    """Weights as a 16-bit path holds them: conv and FC1 filters rounded to
+    ``kind`` (RNE), everything else unchanged."""
     q = dict(weights)
-    q["conv_w"] = to_bf16_rne(weights["conv_w"])
-    q["fc1_w"] = to_bf16_rne(weights["fc1_w"])
+    q["conv_w"] = round16(weights["conv_w"], kind)
+    q["fc1_w"] = round16(weights["fc1_w"], kind)
     return q
 
 
-def forward_bf16_emulated(patches, weights) -> np.ndarray:
-    """Diagnostic: the network with the bf16 path's roundings applied (patch,
-    conv filter, conv output and FC1 filter rounded to bfloat16), accumulated in
-    float64.  Localises a bf16-path discrepancy much more tightly than the
-    full-precision oracle; it is not the grading reference."""
-    q = quantize_bf16_model(weights)
-    P = to_bf16_rne(np.asarray(patches, np.float32))
+def forward_16bit_emulated(patches, weights, kind: str = "bf16") -> np.ndarray:
+    """The network with a 16-bit path's roundings applied — patch, conv filter,
+    conv output (after ReLU) and FC1 filter rounded to ``kind`` — and float64
+    accumulation.  This is what a 16-bit path computes up to its fp32
+    accumulation order; the full-precision ``forward`` remains the reference."""
+    q = quantize_16bit_model(weights, kind)
+    P = round16(np.asarray(patches, np.float32), kind)
     A = conv_relu(P, q["conv_w"], q["conv_b"])
-    A = to_bf16_rne(A.astype(np.float32)).astype(np.float64)
+    A = round16(A.astype(np.float32), kind).astype(np.float64)
     h1 = dense_relu(flatten_hwc(A), q["fc1_w"], q["fc1_b"])
     h2 = dense_relu(h1, q["fc2_w"], q["fc2_b"])
     return heads(h2, q)
+
+
+def forward_bf16_emulated(patches, weights) -> np.ndarray:
+    """``forward_16bit_emulated`` with bfloat16 operands."""
+    return forward_16bit_emulated(patches, weights, "bf16")
+
+
+def classify_16bit_emulated(patches, weights, kind: str, chunk: int = CHUNK) -> np.ndarray:
+    """float32 [n][4] from ``forward_16bit_emulated``, chunked."""
+    patches = np.asarray(patches, dtype=np.float32).reshape(-1, PATCH, PATCH)
+    out = np.empty((patches.shape[0], 4), np.float32)
+    for s in range(0, patches.shape[0], chunk):
+        out[s:s + chunk] = forward_16bit_emulated(patches[s:s + chunk], weights, kind).astype(np.float32)
+    return out

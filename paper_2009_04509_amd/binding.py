@@ -26,6 +26,7 @@ POINTID_ENODEV = -4
 POINTID_EUNSUPPORTED = -5
 POINTID_FP32 = 0
 POINTID_BF16 = 1
+POINTID_FP16 = 2
 MAX_PLANES = 64
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ENODEV", -5: "EUNSUPPORTED"}
@@ -120,7 +121,7 @@ def pointid_timing_query(kernel: str):
 
 def _precision(p) -> int:
     if isinstance(p, str):
-        return {"fp32": POINTID_FP32, "bf16": POINTID_BF16}[p]
+        return {"fp32": POINTID_FP32, "bf16": POINTID_BF16, "fp16": POINTID_FP16}[p]
     return int(p)
 
 
@@ -254,7 +255,7 @@ def pointid_classify_patches(h: Handle, patches: torch.Tensor,
 
 def pointid_gather(image: torch.Tensor, hits: torch.Tensor, out_dtype="fp32",
                    out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """Patches [n][48][48]: float32, or bf16 bit patterns as int16 for ``out_dtype='bf16'``."""
+    """Patches [n][48][48]: float32, or bf16 / fp16 bit patterns as int16."""
     _need(image, torch.float32, "image")
     _need(hits, torch.int32, "hits", None, (2,))
     code = _precision(out_dtype)

@@ -127,9 +127,9 @@ class Workspace {
 constexpr int kSplitsFp32 = 8;            // FC1 split-K on the vector fp32 path
 constexpr int64_t kChunkFp32 = 2048;      // patches whose maps are live at once
 
-// patches (fp32 [n][2304]) -> scores; the shared back half of every classify.
-int run_network(pointid_handle h, const float* patches, int64_t n, float* scores,
-                hipStream_t stream, Workspace& ws) {
+// fp32 handles: patches (fp32 [n][2304]) -> scores.
+int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* scores,
+                     hipStream_t stream, Workspace& ws) {
   const int S = kSplitsFp32;
   float* part = nullptr;
   float* act = nullptr;
@@ -159,21 +159,45 @@ int run_network(pointid_handle h, const float* patches, int64_t n, float* scores
   return POINTID_OK;
 }
 
+// 16-bit handles: patches (bf16 or fp16 [n][2304]) -> scores.
+int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* scores,
+                   hipStream_t stream, Workspace& ws) {
+  const int S = conv_fc1_16_splits();
+  float* part = nullptr;
+  hipError_t e = ws.get(sizeof(float) * (size_t)S * n * kFc1Out, (void**)&part);
+  if (e != hipSuccess) return hip_fail(e, "workspace (FC1 partials)");
+  {
+    KernelTimer kt("conv_fc1_16", stream);
+    e = launch_conv_fc1_16(h->precision == POINTID_FP16, patches, n, 0, n, h->w.fc1_frag,
+                           h->w.conv_frag, part, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "conv_fc1 launch");
+  {
+    KernelTimer kt("tail", stream);
+    e = launch_tail(part, S, n, h->w, scores, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "tail launch");
+  return POINTID_OK;
+}
+
 int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hits,
                   int stride, int64_t n, float* scores, void* stream_) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
   Workspace ws(stream);
-  float* patches = nullptr;
-  hipError_t e = ws.get(sizeof(float) * (size_t)n * kPatchPix, (void**)&patches);
+  const bool half = h->precision != POINTID_FP32;
+  void* patches = nullptr;
+  hipError_t e = ws.get((half ? 2 : 4) * (size_t)n * kPatchPix, &patches);
   if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
   {
     KernelTimer kt("gather", stream);
-    e = launch_gather(planes, hits, stride, n, patches, false, stream);
+    e = launch_gather(planes, hits, stride, n, patches, h->precision, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
-  return run_network(h, patches, n, scores, stream, ws);
+  if (half)
+    return run_network_16(h, static_cast<const uint16_t*>(patches), n, scores, stream, ws);
+  return run_network_fp32(h, static_cast<const float*>(patches), n, scores, stream, ws);
 }
 
 int check_planes(const pointid_plane* planes, int32_t n_planes, PlaneTable* t) {
@@ -251,8 +275,8 @@ int pointid_create(const pointid_weights* w, int precision, int device,
                             w->fc2_b,  w->cls_w,  w->cls_b, w->mic_w, w->mic_b};
   for (const float* m : members)
     if (!m) return fail(POINTID_EINVAL, "a weight pointer is NULL");
-  if (precision != POINTID_FP32)
-    return fail(POINTID_EUNSUPPORTED, "precision not supported by this build");
+  if (precision != POINTID_FP32 && precision != POINTID_BF16 && precision != POINTID_FP16)
+    return fail(POINTID_EUNSUPPORTED, "precision must be POINTID_FP32, POINTID_BF16 or POINTID_FP16");
   int count = 0;
   if (hipGetDeviceCount(&count) != hipSuccess || count <= 0)
     return fail(POINTID_ENODEV, "no HIP device visible");
@@ -274,44 +298,71 @@ int pointid_create(const pointid_weights* w, int precision, int device,
     (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
   }
 
-  struct Piece { const float* src; size_t count; const float** dst; };
   auto* hnd = new (std::nothrow) pointid_s();
   if (!hnd) return fail(POINTID_ENOMEM, "host allocation failed");
   hnd->device = device;
   hnd->precision = precision;
   hnd->w.precision = precision;
-  Piece pieces[] = {
-      {w->conv_w, (size_t)kCh * kK * kK, &hnd->w.conv_w},
-      {w->conv_b, (size_t)kCh, &hnd->w.conv_b},
-      {w->fc1_w, (size_t)kFc1In * kFc1Out, &hnd->w.fc1_w},
-      {w->fc1_b, (size_t)kFc1Out, &hnd->w.fc1_b},
-      {w->fc2_w, (size_t)kFc1Out * kFc2Out, &hnd->w.fc2_w},
-      {w->fc2_b, (size_t)kFc2Out, &hnd->w.fc2_b},
-      {w->cls_w, (size_t)kFc2Out * kNcls, &hnd->w.cls_w},
-      {w->cls_b, (size_t)kNcls, &hnd->w.cls_b},
-      {w->mic_w, (size_t)kFc2Out, &hnd->w.mic_w},
-      {w->mic_b, (size_t)1, &hnd->w.mic_b},
+  const bool half = precision != POINTID_FP32;
+
+  // one device allocation for every tensor the handle keeps
+  struct Piece { const void* src; size_t bytes; const void** dst; };
+  std::vector<Piece> pieces = {
+      {w->conv_w, sizeof(float) * kCh * kK * kK, (const void**)&hnd->w.conv_w},
+      {w->conv_b, sizeof(float) * kCh, (const void**)&hnd->w.conv_b},
+      {w->fc1_b, sizeof(float) * kFc1Out, (const void**)&hnd->w.fc1_b},
+      {w->fc2_w, sizeof(float) * kFc1Out * kFc2Out, (const void**)&hnd->w.fc2_w},
+      {w->fc2_b, sizeof(float) * kFc2Out, (const void**)&hnd->w.fc2_b},
+      {w->cls_w, sizeof(float) * kFc2Out * kNcls, (const void**)&hnd->w.cls_w},
+      {w->cls_b, sizeof(float) * kNcls, (const void**)&hnd->w.cls_b},
+      {w->mic_w, sizeof(float) * kFc2Out, (const void**)&hnd->w.mic_w},
+      {w->mic_b, sizeof(float), (const void**)&hnd->w.mic_b},
   };
+  if (half) {
+    pieces.push_back({nullptr, (size_t)kConvFrags * 16, (const void**)&hnd->w.conv_frag});
+    pieces.push_back({nullptr, (size_t)kFc1Frags * 16, (const void**)&hnd->w.fc1_frag});
+  } else {
+    pieces.push_back({w->fc1_w, sizeof(float) * kFc1In * kFc1Out, (const void**)&hnd->w.fc1_w});
+  }
   size_t total = 0;
   std::vector<size_t> offs;
   for (const Piece& p : pieces) {
     offs.push_back(total);
-    total += (p.count * sizeof(float) + 255) & ~size_t(255);
+    total += (p.bytes + 255) & ~size_t(255);
   }
   e = hipMalloc(&hnd->blob, total);
   if (e != hipSuccess) {
     delete hnd;
     return hip_fail(e, "hipMalloc(weights)");
   }
-  for (size_t i = 0; i < sizeof(pieces) / sizeof(pieces[0]); ++i) {
+  for (size_t i = 0; i < pieces.size(); ++i) {
     char* d = static_cast<char*>(hnd->blob) + offs[i];
-    e = hipMemcpy(d, pieces[i].src, pieces[i].count * sizeof(float), hipMemcpyHostToDevice);
+    *pieces[i].dst = d;
+    if (!pieces[i].src) continue;            // filled on the device below
+    e = hipMemcpy(d, pieces[i].src, pieces[i].bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       (void)hipFree(hnd->blob);
       delete hnd;
       return hip_fail(e, "hipMemcpy(weights)");
     }
-    *pieces[i].dst = reinterpret_cast<const float*>(d);
+  }
+  if (half) {
+    // 16-bit fragments are packed on the device from a temporary fp32 FC1 copy
+    float* w1 = nullptr;
+    e = hipMalloc(&w1, sizeof(float) * kFc1In * kFc1Out);
+    if (e == hipSuccess)
+      e = hipMemcpy(w1, w->fc1_w, sizeof(float) * kFc1In * kFc1Out, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = launch_pack_16(precision == POINTID_FP16, hnd->w.conv_w, hnd->w.conv_b, w1,
+                         const_cast<uint4*>(hnd->w.conv_frag), const_cast<uint4*>(hnd->w.fc1_frag),
+                         nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (w1) (void)hipFree(w1);
+    if (e != hipSuccess) {
+      (void)hipFree(hnd->blob);
+      delete hnd;
+      return hip_fail(e, "weight packing");
+    }
   }
   *out = hnd;
   return POINTID_OK;
@@ -375,7 +426,16 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
   Workspace ws(stream);
-  return run_network(h, patches, n, scores, stream, ws);
+  if (h->precision == POINTID_FP32) return run_network_fp32(h, patches, n, scores, stream, ws);
+  uint16_t* pb = nullptr;
+  hipError_t e = ws.get(2 * (size_t)n * kPatchPix, (void**)&pb);
+  if (e != hipSuccess) return hip_fail(e, "workspace (16-bit patches)");
+  {
+    KernelTimer kt("patches_to_16", stream);
+    e = launch_patches_to_16(h->precision == POINTID_FP16, patches, n, pb, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "16-bit cast launch");
+  return run_network_16(h, pb, n, scores, stream, ws);
 }
 
 int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,
@@ -383,8 +443,8 @@ int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,
                    int out_dtype, void* stream) {
   if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
   if (n_wires <= 0 || n_ticks <= 0) return fail(POINTID_EINVAL, "n_wires and n_ticks must be positive");
-  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16)
-    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32 or POINTID_BF16");
+  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16 && out_dtype != POINTID_FP16)
+    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32, POINTID_BF16 or POINTID_FP16");
   if (n_hits == 0) return POINTID_OK;
   if (!image || !hits || !patches_out) return fail(POINTID_EINVAL, "NULL device pointer");
   if (!aligned16(patches_out)) return fail(POINTID_EINVAL, "patches_out must be 16-byte aligned");
@@ -392,7 +452,7 @@ int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,
   std::memset(&t, 0, sizeof(t));
   t.n = 1;
   t.p[0] = {image, n_wires, n_ticks};
-  hipError_t e = launch_gather(t, hits, 2, n_hits, patches_out, out_dtype == POINTID_BF16,
+  hipError_t e = launch_gather(t, hits, 2, n_hits, patches_out, out_dtype,
                                static_cast<hipStream_t>(stream));
   return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
 }
@@ -400,15 +460,15 @@ int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,
 int pointid_gather_planes(const pointid_plane* planes, int32_t n_planes, const int32_t* hits,
                           int64_t n_hits, void* patches_out, int out_dtype, void* stream) {
   if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
-  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16)
-    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32 or POINTID_BF16");
+  if (out_dtype != POINTID_FP32 && out_dtype != POINTID_BF16 && out_dtype != POINTID_FP16)
+    return fail(POINTID_EUNSUPPORTED, "out_dtype must be POINTID_FP32, POINTID_BF16 or POINTID_FP16");
   PlaneTable t;
   int rc = check_planes(planes, n_planes, &t);
   if (rc != POINTID_OK) return rc;
   if (n_hits == 0) return POINTID_OK;
   if (!hits || !patches_out) return fail(POINTID_EINVAL, "NULL device pointer");
   if (!aligned16(patches_out)) return fail(POINTID_EINVAL, "patches_out must be 16-byte aligned");
-  hipError_t e = launch_gather(t, hits, 3, n_hits, patches_out, out_dtype == POINTID_BF16,
+  hipError_t e = launch_gather(t, hits, 3, n_hits, patches_out, out_dtype,
                                static_cast<hipStream_t>(stream));
   return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
 }

@@ -9,9 +9,11 @@
 //      row from LDS at the row's misalignment offset and writes one aligned
 //      16-byte store, so a wavefront writes 1 KiB of contiguous output per
 //      instruction.
-// Values are copied, never computed (bf16 output is round-to-nearest-even of
-// the fp32 pixel), so the result is bit-exact.
+// Values are copied, never computed (bf16 / fp16 output is the
+// round-to-nearest-even of the fp32 pixel), so the result is bit-exact.
+#include "pointid.h"
 #include "internal.h"
+#include "op16.h"
 
 namespace pointid {
 namespace {
@@ -20,17 +22,9 @@ constexpr int kWaves = 4;                 // patches per block (one per wave)
 constexpr int kChunks = 13;               // 16-byte chunks staged per row
 constexpr int kStageCols = kChunks * 4;   // 52 floats
 
-__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
-  // round to nearest, ties to even: add 0x7FFF plus the lowest kept bit,
-  // then keep the upper half (finite inputs)
-  uint32_t u = __float_as_uint(x);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
 __device__ __forceinline__ int64_t mod4(int64_t x) { return ((x % 4) + 4) % 4; }
 
-template <bool kBf16>
+template <int kOut>
 __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
                                                      const int32_t* __restrict__ hits,
                                                      int hit_stride, int64_t n,
@@ -96,7 +90,7 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
   if (!active) return;
 
   // ---- emit
-  if constexpr (!kBf16) {
+  if constexpr (kOut == POINTID_FP32) {
     float4* o = reinterpret_cast<float4*>(static_cast<float*>(out) + i * kPatchPix);
     for (int k = lane; k < kPatch * 12; k += 64) {
       const int r = k / 12;
@@ -116,29 +110,52 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
       const int off = (plane_ok && wire >= 0 && wire < W)
                           ? (int)mod4((int64_t)wire * T + (t - kHalf)) : 0;
       const float* s = &st[r][off + c];
-      uint4 v;
-      v.x = bf16_rne_bits(s[0]) | (bf16_rne_bits(s[1]) << 16);
-      v.y = bf16_rne_bits(s[2]) | (bf16_rne_bits(s[3]) << 16);
-      v.z = bf16_rne_bits(s[4]) | (bf16_rne_bits(s[5]) << 16);
-      v.w = bf16_rne_bits(s[6]) | (bf16_rne_bits(s[7]) << 16);
-      o[k] = v;
+      using Op = Op16<kOut == POINTID_FP16>;
+      o[k] = make_uint4(Op::pack(s[0], s[1]), Op::pack(s[2], s[3]), Op::pack(s[4], s[5]),
+                        Op::pack(s[6], s[7]));
     }
   }
 }
 
+// Elementwise fp32 -> 16-bit (RNE) for pre-cut patches: 8 values per thread.
+template <bool kFp16>
+__global__ __launch_bounds__(256) void to_16_kernel(const float4* __restrict__ in, int64_t n8,
+                                                    uint4* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const float4 a = in[2 * i], b = in[2 * i + 1];
+  using Op = Op16<kFp16>;
+  out[i] = make_uint4(Op::pack(a.x, a.y), Op::pack(a.z, a.w), Op::pack(b.x, b.y),
+                      Op::pack(b.z, b.w));
+}
+
 }  // namespace
 
+hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t* out,
+                                hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t n8 = n * kPatchPix / 8;
+  const dim3 grid((unsigned)((n8 + 255) / 256));
+  if (fp16)
+    to_16_kernel<true><<<grid, dim3(256), 0, stream>>>(reinterpret_cast<const float4*>(in), n8,
+                                                      reinterpret_cast<uint4*>(out));
+  else
+    to_16_kernel<false><<<grid, dim3(256), 0, stream>>>(reinterpret_cast<const float4*>(in), n8,
+                                                       reinterpret_cast<uint4*>(out));
+  return hipGetLastError();
+}
+
 hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
-                         int hit_stride, int64_t n, void* out, bool out_bf16,
+                         int hit_stride, int64_t n, void* out, int out_dtype,
                          hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  const int64_t blocks = (n + kWaves - 1) / kWaves;
-  if (out_bf16)
-    gather_kernel<true><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        planes, hits, hit_stride, n, out);
+  const dim3 grid((unsigned)((n + kWaves - 1) / kWaves));
+  if (out_dtype == POINTID_BF16)
+    gather_kernel<POINTID_BF16><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
+  else if (out_dtype == POINTID_FP16)
+    gather_kernel<POINTID_FP16><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
   else
-    gather_kernel<false><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        planes, hits, hit_stride, n, out);
+    gather_kernel<POINTID_FP32><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
   return hipGetLastError();
 }
 

@@ -36,7 +36,7 @@ struct PlaneTable {
 // Device-resident parameters of one handle.  fp32 tensors are in the ABI
 // layouts; packed tensors are in the layouts the MFMA kernels read.
 struct DeviceWeights {
-  int precision;             // POINTID_FP32 / POINTID_BF16
+  int precision;             // POINTID_FP32 / POINTID_BF16 / POINTID_FP16
   const float* conv_w;       // [48][25] fp32
   const float* conv_b;       // [48]
   const float* fc1_w;        // [92928][128] fp32 (fp32 handles)
@@ -47,13 +47,37 @@ struct DeviceWeights {
   const float* cls_b;        // [3]
   const float* mic_w;        // [32]
   const float* mic_b;        // [1]
+  // 16-bit handles: MFMA operand fragments (see conv_fc1_16.hip)
+  const uint4* conv_frag;    // [2 shifts][3 channel tiles][64 lanes] x 8 halves
+  const uint4* fc1_frag;     // [968 pairs][3 K-steps][8 output tiles][64 lanes] x 8 halves
 };
 
+// Fragment counts of the 16-bit packed weights.
+constexpr int64_t kConvFrags = 2 * 3 * 64;
+constexpr int64_t kFc1Frags = (int64_t)(kPos / 2) * 3 * 8 * 64;
+
 // Patch construction.  hits: int32 rows of `hit_stride` (2 = (wire, tick) on
-// plane 0, 3 = (plane, wire, tick)).  out: [n][48][48] fp32 or bf16 bits.
+// plane 0, 3 = (plane, wire, tick)).  out: [n][48][48] of `out_dtype`
+// (POINTID_FP32, or POINTID_BF16 / POINTID_FP16 bit patterns, RNE).
 hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
-                         int hit_stride, int64_t n, void* out, bool out_bf16,
+                         int hit_stride, int64_t n, void* out, int out_dtype,
                          hipStream_t stream);
+
+// Round fp32 patches [n][2304] to bf16 or fp16 (RNE) bit patterns.
+hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t* out,
+                                hipStream_t stream);
+
+// Repack fp32 conv/FC1 weights into 16-bit MFMA fragments.
+hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
+                          const float* fc1_w, uint4* conv_frag, uint4* fc1_frag,
+                          hipStream_t stream);
+
+// Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
+// bits) -> part[s][row0 + i][128] for s < conv_fc1_16_splits().
+int conv_fc1_16_splits();
+hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int64_t row0,
+                              int64_t n_total, const uint4* w1p, const uint4* convp,
+                              float* part, hipStream_t stream);
 
 // fp32 conv + ReLU for patches [n][2304] -> activations [n][92928] (HWC).
 hipError_t launch_conv_fp32(const float* patches, int64_t n,

@@ -125,6 +125,15 @@ def test_bf16_rne_matches_torch():
                           (ref.view(np.uint32) >> 16).astype(np.uint16))
 
 
+def test_fp16_rne_matches_torch():
+    rng = np.random.default_rng(10)
+    x = (rng.standard_normal(100000) * 10 ** rng.uniform(-9, 4.8, 100000)).astype(np.float32)
+    x = np.concatenate([x, np.float32([0.0, -0.0, 1.0, 65504.0, 6.1e-5, 5.96e-8, 2.9e-8, 3e-8])])
+    ref = torch.from_numpy(x).to(torch.float16)
+    assert np.array_equal(oracle.fp16_bits(x), ref.view(torch.int16).numpy().view(np.uint16))
+    assert np.array_equal(oracle.to_fp16_rne(x), ref.to(torch.float32).numpy())
+
+
 # ---------------------------------------------------------------- convolution
 
 def _conv_bruteforce(P, K, b):
@@ -313,11 +322,20 @@ def test_planes_match_single_plane():
     assert np.array_equal(s[len(b.hits):], oracle.classify(a.image, a.hits, w))
 
 
-def test_bf16_emulation_close_to_full_precision():
-    """The diagnostic bf16-rounded network stays within the bf16 budget of the
-    full-precision oracle on these inputs (sanity of the diagnostic only)."""
+def test_16bit_emulation_rounds_the_right_operands():
+    """The 16-bit emulation equals the full network when every rounded operand
+    is already representable, and moves away from it otherwise."""
     w = synth.he_normal_weights()
-    P = synth.config4_patches(32, seed=9)
-    full = oracle.forward(P, w)
-    emu = oracle.forward_bf16_emulated(P, w)
-    assert np.max(np.abs(full - emu)) < 2e-2
+    P = synth.config4_patches(8, seed=9)
+    for kind in ("bf16", "fp16"):
+        q = oracle.quantize_16bit_model(w, kind)
+        # representable patch and weights: only the conv output rounding remains
+        Pq = oracle.round16(P, kind)
+        A = oracle.conv_relu(Pq, q["conv_w"], q["conv_b"])
+        Aq = oracle.round16(A.astype(np.float32), kind).astype(np.float64)
+        h1 = oracle.dense_relu(oracle.flatten_hwc(Aq), q["fc1_w"], q["fc1_b"])
+        h2 = oracle.dense_relu(h1, q["fc2_w"], q["fc2_b"])
+        np.testing.assert_array_equal(oracle.heads(h2, q), oracle.forward_16bit_emulated(P, w, kind))
+        full = oracle.forward(P, w)
+        d = np.abs(full - oracle.forward_16bit_emulated(P, w, kind)).max()
+        assert 0 < d < 2e-2
