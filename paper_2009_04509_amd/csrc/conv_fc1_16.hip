@@ -2,20 +2,22 @@
 // with bf16 or fp16 operands and fp32 accumulation.
 //
 // FC1 is a skinny, very deep GEMM (M = patches, N = 128, K = 92,928) whose A
-// operand — the conv maps, 185,856 B per patch in bf16 — would cost twice its
+// operand — the conv maps, 185,856 B per patch in 16 bits — would cost twice its
 // size in HBM traffic if written out and read back.  Here the conv is FC1's
 // operand producer: the maps exist only in registers.
 //
-// Work split.  A block owns 128 patches and one of kSplits contiguous ranges of
+// Work split.  A block owns 96 patches and one of kSplits contiguous ranges of
 // map positions (split-K); blockIdx % 8 selects the range, so every block on one
 // XCD reads the same 1/8 of the FC1 weights and that slice (2.97 MB) stays in
 // the XCD's 4 MB L2.  Positions are taken in pairs (x, x+1) with x even: the
 // 5x6 pixel window of a pair (30 values) fits one K=32 MFMA operand, shared by
-// both positions.  The block's four waves take interleaved pairs; each wave
-// accumulates all 128 outputs for all 128 patches (8 x 8 tiles of 16x16, 256
-// accumulator registers), so an FC1 weight fragment fetched from L2 is used for
-// 8 MFMAs and no weight goes through LDS.  LDS holds a ring of 8 patch rows
-// (the 5 rows a map row needs, plus the next) for the block's 128 patches.
+// both positions.  The block's 8 waves (2 per SIMD, so one wave's conversions
+// overlap the other's MFMAs) form 4 position groups x 2 output halves: the two
+// waves of a group take the same interleaved pairs and the same 96 patches, and
+// each accumulates 64 of the 128 outputs (4 x 6 tiles of 16x16).  Both compute
+// the conv of their pair; each FC1 weight fragment fetched from L2 feeds 6
+// MFMAs and no weight goes through LDS.  LDS holds a ring of 8 patch rows (the 5
+// rows a map row needs, plus the next) for the block's 96 patches.
 //
 // Per pair and per 16-patch tile, v_mfma_f32_16x16x32_{bf16,f16}:
 //   conv:  D[ch][patch] = sum_slot Kc[ch][slot] * Win[slot][patch]
@@ -31,69 +33,86 @@
 //   time into the matching K order, one 1 KiB fragment per (pair, step, 16 outputs).
 //   FC1:   acc[n][patch] += W1t[n][k] * maps[k][patch]
 //
-// The block's four partial sums are added in LDS in a fixed order and written
-// as fp32 partials [split][patch][128]; the tail kernel adds the splits.
+// The four position groups' partial sums are added in LDS in a fixed order and
+// written as fp32 partials [split][patch][128]; the tail kernel adds the splits.
 #include "internal.h"
 #include "op16.h"
 
 namespace pointid {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kBt = 112;                    // patches per block (7 MFMA tiles)
-constexpr int kTiles = kBt / 16;            // 16-patch MFMA tiles per wave
-constexpr int kPairsPerRow = kFm / 2;       // 22
-constexpr int kRing = 8;                    // patch-row ring slots
-constexpr int kRP = 26;                     // LDS row pitch, dwords (24 used)
-constexpr int kSlot = kBt * kRP;            // dwords per ring slot
-constexpr int kLdsDwords = 2 * 64 * 256;    // 128 KiB: ring (104 KiB) / reduction (128 KiB)
-// One patch row (96 B) of each of the block's patches: kBt x 6 chunks of 16 B,
-// at most 3 per thread.
-constexpr int kRowChunks = kBt * 6;
+constexpr int kKGroups = 4;                   // position groups (interleaved pairs)
+constexpr int kNHalves = 2;                   // output halves
+constexpr int kWaves = kKGroups * kNHalves;   // 8
+constexpr int kThreads = kWaves * 64;         // 512
+constexpr int kMT = 8 / kNHalves;             // 16-output tiles per wave
+constexpr int kBt = 96;                       // patches per block
+constexpr int kTiles = kBt / 16;              // 16-patch MFMA tiles
+constexpr int kPairsPerRow = kFm / 2;         // 22
+constexpr int kRing = 8;                      // patch-row ring slots
+constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
+constexpr int kSlot = kBt * kRP;              // dwords per ring slot
+constexpr int kRegion = kMT * kTiles * 4 * 64;          // one wave's partial sums (floats)
+constexpr int kLdsDwords = (kRing * kSlot > 4 * kRegion) ? kRing * kSlot : 4 * kRegion;
 
-__device__ __forceinline__ void row_load(const uint16_t* __restrict__ patches, int64_t n,
-                                         int64_t p_base, int r, uint4 (&v)[3]) {
-#pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    const int c = threadIdx.x + 256 * k;
-    const int p = c / 6, h = c - (c / 6) * 6;
-    const int64_t gp = p_base + p;
-    v[k] = (c < kRowChunks && gp < n)
-               ? *reinterpret_cast<const uint4*>(patches + gp * kPatchPix + r * kPatch + h * 8)
-               : make_uint4(0u, 0u, 0u, 0u);
-  }
+// One patch row (96 B) of each of the block's patches: kBt x 6 chunks of 16 B.
+// Chunk c = tid, plus c = kThreads + tid for the first kRowExtra threads (whole
+// waves, so no lane diverges).  Patches past the end of the batch are read from
+// the last patch instead: their results are never stored.
+constexpr int kRowChunks = kBt * 6;
+constexpr int kRowExtra = kRowChunks - kThreads;
+static_assert(kRowExtra > 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads, "row chunking");
+
+__device__ __forceinline__ uint4 row_chunk_load(const uint16_t* __restrict__ patches, int64_t n,
+                                                int64_t p_base, int r, int c) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int p = c / 6, h = c - (c / 6) * 6;
+  int64_t gp = p_base + p;
+  gp = gp < n ? gp : n - 1;
+  // streamed once per block: non-temporal, so it does not push the block's FC1
+  // weight slice out of L2
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+                                       patches + gp * kPatchPix + r * kPatch + h * 8)));
 }
 
-__device__ __forceinline__ void row_store(uint32_t* lds, int r, const uint4 (&v)[3]) {
-  const int slot = r & (kRing - 1);
-#pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    const int c = threadIdx.x + 256 * k;
-    if (c >= kRowChunks) break;
-    const int p = c / 6, h = c - (c / 6) * 6;
-    uint32_t* d = lds + slot * kSlot + p * kRP + h * 4;
-    *reinterpret_cast<uint2*>(d) = make_uint2(v[k].x, v[k].y);
-    *reinterpret_cast<uint2*>(d + 2) = make_uint2(v[k].z, v[k].w);
-  }
+__device__ __forceinline__ void row_chunk_store(uint32_t* lds, int r, int c, const uint4& v) {
+  const int p = c / 6, h = c - (c / 6) * 6;
+  uint32_t* d = lds + (r & (kRing - 1)) * kSlot + p * kRP + h * 4;
+  *reinterpret_cast<uint2*>(d) = make_uint2(v.x, v.y);
+  *reinterpret_cast<uint2*>(d + 2) = make_uint2(v.z, v.w);
+}
+
+__device__ __forceinline__ void row_load(const uint16_t* __restrict__ patches, int64_t n,
+                                         int64_t p_base, int r, bool extra, uint4 (&v)[2]) {
+  v[0] = row_chunk_load(patches, n, p_base, r, threadIdx.x);
+  if (extra) v[1] = row_chunk_load(patches, n, p_base, r, threadIdx.x + kThreads);
+}
+
+__device__ __forceinline__ void row_store(uint32_t* lds, int r, bool extra, const uint4 (&v)[2]) {
+  row_chunk_store(lds, r, threadIdx.x, v[0]);
+  if (extra) row_chunk_store(lds, r, threadIdx.x + kThreads, v[1]);
 }
 
 template <bool kFp16, int kSplits>
-__global__ __launch_bounds__(256, 1) void conv_fc1_16_kernel(
+__global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     const uint16_t* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
     const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[kLdsDwords];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave % kKGroups;            // position group
+  const int nh = wave / kKGroups;            // output half
+  const bool extra = wave < kRowExtra / 64;  // wave-uniform
   const int col = lane & 15;                 // MFMA column (patch within tile) / row
   const int grp = lane >> 4;                 // MFMA K-slot group
   const int split = blockIdx.x % kSplits;
   const int64_t p_base = (int64_t)(blockIdx.x / kSplits) * kBt;
-  // split boundaries on whole steps of 4 pairs, so every wave runs `steps` pairs
-  constexpr int kGroups = kPos / 2 / kWaves;            // 242
+  // split boundaries on whole steps of kKGroups pairs: every wave runs `steps` pairs
+  constexpr int kGroups = kPos / 2 / kKGroups;          // 242
   const int G0 = (kGroups * split) / kSplits;
   const int steps = (kGroups * (split + 1)) / kSplits - G0;
-  const int P0 = kWaves * G0;
+  const int P0 = kKGroups * G0;
 
   // conv filter fragments: [shift][channel tile]
   uint4 cw[2][3];
@@ -114,38 +133,48 @@ __global__ __launch_bounds__(256, 1) void conv_fc1_16_kernel(
   const bool const_slot = (grp == 3);
   using Op = Op16<kFp16>;
 
-  floatx4 acc[8][kTiles];
+  floatx4 acc[kMT][kTiles];
 #pragma unroll
-  for (int m = 0; m < 8; ++m)
+  for (int m = 0; m < kMT; ++m)
 #pragma unroll
     for (int i = 0; i < kTiles; ++i) acc[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
   // ---- initial patch rows
   auto top_row = [&](int step) {             // highest input row needed by a step
-    return (P0 + kWaves * step + kWaves - 1) / kPairsPerRow + kK - 1;
+    return (P0 + kKGroups * step + kKGroups - 1) / kPairsPerRow + kK - 1;
   };
   int loaded_hi = top_row(0);
   for (int r = P0 / kPairsPerRow; r <= loaded_hi; ++r) {
-    uint4 v[3];
-    row_load(patches, n, p_base, r, v);
-    row_store(lds, r, v);
+    uint4 v[2];
+    row_load(patches, n, p_base, r, extra, v);
+    row_store(lds, r, extra, v);
   }
   __syncthreads();
 
-  const uint4* wl = w1p + lane;
-  uint4 wcur[8];
+  // FC1 fragments through a buffer resource: the fragment base is a scalar
+  // offset and the output tiles are immediate offsets, so the loads need no
+  // per-lane address arithmetic; reads past the end return 0.
+  const __amdgpu_buffer_rsrc_t w1r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(w1p), (short)0, (int)(kFc1Frags * 16), 0x00020000);
+  const int voff = lane * 16 + nh * kMT * 1024;
+  auto load_w = [&](int P, int q, uint4 (&w)[kMT]) {
+    const int so = (P * 3 + q) * 8 * 1024;
 #pragma unroll
-  for (int m = 0; m < 8; ++m) wcur[m] = wl[(((P0 + wave) * 3 + 0) * 8 + m) * 64];
+    for (int m = 0; m < kMT; ++m)
+      w[m] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(w1r, voff + m * 1024, so, 0));
+  };
+  uint4 wcur[kMT];
+  load_w(P0 + kg, 0, wcur);
 
 #pragma unroll 1
   for (int step = 0; step < steps; ++step) {
     // prefetch the patch row the next step adds (at most one; block-uniform)
-    uint4 rv[3];
+    uint4 rv[2];
     const int next_hi = (step + 1 < steps) ? top_row(step + 1) : loaded_hi;
     const bool new_row = next_hi > loaded_hi;
-    if (new_row) row_load(patches, n, p_base, next_hi, rv);
+    if (new_row) row_load(patches, n, p_base, next_hi, extra, rv);
 
-    const int P = P0 + kWaves * step + wave;
+    const int P = P0 + kKGroups * step + kg;
     const int y = P / kPairsPerRow;
     const int xh = P - y * kPairsPerRow;     // x / 2
     uint4 win[kTiles];
@@ -165,13 +194,14 @@ __global__ __launch_bounds__(256, 1) void conv_fc1_16_kernel(
     }
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
-      // prefetch the next FC1 weight step of this wave (clamped past the end)
-      int Pn = (q < 2) ? P : P + kWaves;
+      // prefetch the next FC1 weight step of this wave (past the end reads 0)
+      const int Pn = (q < 2) ? P : P + kKGroups;
       const int qn = (q < 2) ? q + 1 : 0;
-      if (Pn > kPos / 2 - 1) Pn = kPos / 2 - 1;
-      uint4 wnext[8];
-#pragma unroll
-      for (int m = 0; m < 8; ++m) wnext[m] = wl[((Pn * 3 + qn) * 8 + m) * 64];
+      uint4 wnext[kMT];
+      load_w(Pn, qn, wnext);
+      // keep these loads here: the scheduler would otherwise sink them to their
+      // use in the next step and expose the full memory latency
+      __builtin_amdgcn_sched_barrier(0);
       // conv tiles feeding this K=32 step: (shift, channel tile)
       const int sa = (q == 2) ? 1 : 0, ta = (q == 0) ? 0 : (q == 1 ? 2 : 1);
       const int sb = (q == 0) ? 0 : 1, tb = (q == 0) ? 1 : (q == 1 ? 0 : 2);
@@ -183,56 +213,62 @@ __global__ __launch_bounds__(256, 1) void conv_fc1_16_kernel(
         const uint4 bf = make_uint4(relu2(Op::pack(ca[0], ca[1])), relu2(Op::pack(ca[2], ca[3])),
                                     relu2(Op::pack(cb[0], cb[1])), relu2(Op::pack(cb[2], cb[3])));
 #pragma unroll
-        for (int m = 0; m < 8; ++m) acc[m][i] = Op::mfma(wcur[m], bf, acc[m][i]);
+        for (int m = 0; m < kMT; ++m) acc[m][i] = Op::mfma(wcur[m], bf, acc[m][i]);
       }
 #pragma unroll
-      for (int m = 0; m < 8; ++m) wcur[m] = wnext[m];
+      for (int m = 0; m < kMT; ++m) wcur[m] = wnext[m];
     }
+    // The ring slot a new row overwrites held row next_hi - 8, which is below
+    // every row the steps since the last barrier read, so waves may drift
+    // apart between row loads; the barrier publishes the new row before any
+    // wave's next step reads it.  (new_row is block-uniform.)
     if (new_row) {
-      row_store(lds, next_hi, rv);
+      row_store(lds, next_hi, extra, rv);
       loaded_hi = next_hi;
+      __syncthreads();
     }
-    __syncthreads();
   }
+  __syncthreads();
 
-  // ---- fixed-order reduction of the four waves: (w0 + w2) + (w1 + w3)
+  // ---- fixed-order reduction over position groups, per output half:
+  //      (g0 + g2) + (g1 + g3)
   float* red = reinterpret_cast<float*>(lds);
   auto put = [&](int region) {
 #pragma unroll
-    for (int m = 0; m < 8; ++m)
+    for (int m = 0; m < kMT; ++m)
 #pragma unroll
       for (int i = 0; i < kTiles; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          red[region * 16384 + ((m * kTiles + i) * 4 + e) * 64 + lane] = acc[m][i][e];
+          red[region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane] = acc[m][i][e];
   };
   auto add = [&](int region) {
 #pragma unroll
-    for (int m = 0; m < 8; ++m)
+    for (int m = 0; m < kMT; ++m)
 #pragma unroll
       for (int i = 0; i < kTiles; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          acc[m][i][e] += red[region * 16384 + ((m * kTiles + i) * 4 + e) * 64 + lane];
+          acc[m][i][e] += red[region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane];
   };
-  if (wave >= 2) put(wave - 2);
+  if (kg >= 2) put(nh * 2 + (kg - 2));
   __syncthreads();
-  if (wave < 2) add(wave);
+  if (kg < 2) add(nh * 2 + kg);
   __syncthreads();
-  if (wave == 1) put(0);
+  if (kg == 1) put(nh);
   __syncthreads();
-  if (wave != 0) return;
-  add(0);
+  if (kg != 0) return;
+  add(nh);
 
-  // acc[m][i]: outputs 16m + 4*grp + e for patch 16i + col
+  // acc[m][i]: outputs 16(nh*kMT + m) + 4*grp + e for patch 16i + col
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
 #pragma unroll
   for (int i = 0; i < kTiles; ++i) {
     const int64_t p = (int64_t)i * 16 + col;
     if (p_base + p < n) {
 #pragma unroll
-      for (int m = 0; m < 8; ++m)
-        *reinterpret_cast<floatx4*>(dst + p * kFc1Out + 16 * m + 4 * grp) = acc[m][i];
+      for (int m = 0; m < kMT; ++m)
+        *reinterpret_cast<floatx4*>(dst + p * kFc1Out + 16 * (nh * kMT + m) + 4 * grp) = acc[m][i];
     }
   }
 }
@@ -250,10 +286,10 @@ hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int
   const int64_t tiles = (n + kBt - 1) / kBt;
   const dim3 grid((unsigned)(tiles * kSplits16));
   if (fp16)
-    conv_fc1_16_kernel<true, kSplits16><<<grid, dim3(256), 0, stream>>>(
+    conv_fc1_16_kernel<true, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
         patches, n, w1p, convp, part, row0, n_total);
   else
-    conv_fc1_16_kernel<false, kSplits16><<<grid, dim3(256), 0, stream>>>(
+    conv_fc1_16_kernel<false, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
         patches, n, w1p, convp, part, row0, n_total);
   return hipGetLastError();
 }

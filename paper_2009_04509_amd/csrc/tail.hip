@@ -2,74 +2,97 @@
 // h1 = ReLU(b1 + sum_s part[s]), h2 = ReLU(b2 + h1 W2), then the softmax
 // branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
-// One wavefront handles 64 patches.  The partials are summed in ascending
-// split order by the thread that owns each element, so the result does not
-// depend on scheduling.  W2 and the head weights are broadcast from LDS; each
-// lane then evaluates one patch.
+// A block of 256 threads handles 64 patches.
+//   1. Each thread owns one float4 column slice of 8 patch rows and sums the
+//      partials in ascending split order (coalesced 512 B rows), adds b1,
+//      applies ReLU and stores h1 in LDS.
+//   2. A group of 32 lanes evaluates one patch at a time: lane j keeps column j
+//      of W2 in registers and forms h2[j] from h1 broadcast out of LDS; the
+//      four head inputs are reduced across the 32 lanes by a fixed butterfly.
+// Every patch is computed by the same instruction sequence whatever its
+// position, so results do not depend on the batch or the hit order.
 #include "internal.h"
 
 namespace pointid {
 namespace {
 
-constexpr int kRows = 64;
+constexpr int kRows = 64;                  // patches per block
+constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 
-__global__ __launch_bounds__(64) void tail_kernel(const float* __restrict__ part, int splits,
-                                                  int64_t n, DeviceWeights w,
-                                                  float* __restrict__ scores) {
-  __shared__ float H[kRows][kFc1Out + 1];
-  __shared__ float W2[kFc1Out][kFc2Out];
-  __shared__ float Hd[kFc2Out][4];     // cls_w (3) | mic_w
-  __shared__ float B1[kFc1Out];
-  __shared__ float B2[kFc2Out];
+__device__ __forceinline__ float sum32(float v) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) v += __shfl_xor(v, m, 32);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
+                                                   int64_t n, DeviceWeights w,
+                                                   float* __restrict__ scores) {
+  __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
   const int tid = threadIdx.x;
   const int64_t p0 = (int64_t)blockIdx.x * kRows;
-  const int rows = (int)((n - p0) < kRows ? (n - p0) : kRows);
 
-  for (int i = tid; i < kFc1Out * kFc2Out; i += 64) W2[i / kFc2Out][i % kFc2Out] = w.fc2_w[i];
-  for (int i = tid; i < kFc1Out; i += 64) B1[i] = w.fc1_b[i];
-  if (tid < kFc2Out) {
-    B2[tid] = w.fc2_b[tid];
-    Hd[tid][0] = w.cls_w[tid * 3 + 0];
-    Hd[tid][1] = w.cls_w[tid * 3 + 1];
-    Hd[tid][2] = w.cls_w[tid * 3 + 2];
-    Hd[tid][3] = w.mic_w[tid];
+  // ---- 1. fixed-order split-K reduction, + b1, ReLU
+  {
+    const int c4 = tid & 31;                 // float4 column
+    const int r0 = tid >> 5;                 // rows r0, r0 + 8, ...
+    float4 acc[kRows / 8];
+#pragma unroll
+    for (int k = 0; k < kRows / 8; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < splits; ++s) {
+      const float4* src = reinterpret_cast<const float4*>(part + ((int64_t)s * n + p0) * kFc1Out);
+#pragma unroll
+      for (int k = 0; k < kRows / 8; ++k) {
+        const int r = r0 + 8 * k;
+        if (p0 + r < n) {
+          const float4 v = src[r * (kFc1Out / 4) + c4];
+          acc[k].x += v.x;
+          acc[k].y += v.y;
+          acc[k].z += v.z;
+          acc[k].w += v.w;
+        }
+      }
+    }
+    const float4 b = reinterpret_cast<const float4*>(w.fc1_b)[c4];
+#pragma unroll
+    for (int k = 0; k < kRows / 8; ++k) {
+      const int r = r0 + 8 * k;
+      *reinterpret_cast<float4*>(&H[r][4 * c4]) =
+          make_float4(fmaxf(acc[k].x + b.x, 0.f), fmaxf(acc[k].y + b.y, 0.f),
+                      fmaxf(acc[k].z + b.z, 0.f), fmaxf(acc[k].w + b.w, 0.f));
+    }
   }
   __syncthreads();
 
-  // fixed-order split-K reduction (each element owned by one thread)
-  for (int idx = tid; idx < rows * kFc1Out; idx += 64) {
-    const int r = idx >> 7, c = idx & 127;
-    const float* src = part + (p0 + r) * kFc1Out + c;
-    float s = src[0];
-    for (int q = 1; q < splits; ++q) s += src[(int64_t)q * n * kFc1Out];
-    H[r][c] = fmaxf(s + B1[c], 0.f);
-  }
-  __syncthreads();
-  if (tid >= rows) return;
-
-  float h2[kFc2Out];
+  // ---- 2. FC2 + heads, 32 lanes per patch
+  const int j = tid & 31;
+  const int grp = tid >> 5;                  // 8 groups
+  float wc[kFc1Out];
 #pragma unroll
-  for (int j = 0; j < kFc2Out; ++j) h2[j] = 0.f;
-  for (int i = 0; i < kFc1Out; ++i) {
-    const float hv = H[tid][i];
+  for (int i = 0; i < kFc1Out; ++i) wc[i] = w.fc2_w[i * kFc2Out + j];
+  const float b2 = w.fc2_b[j];
+  const float c0 = w.cls_w[j * 3 + 0], c1 = w.cls_w[j * 3 + 1], c2 = w.cls_w[j * 3 + 2];
+  const float mw = w.mic_w[j];
+  const float cb0 = w.cls_b[0], cb1 = w.cls_b[1], cb2 = w.cls_b[2], mb = w.mic_b[0];
+  for (int r = grp; r < kRows; r += 8) {
+    if (p0 + r >= n) break;
+    float h = 0.f;
 #pragma unroll
-    for (int j = 0; j < kFc2Out; ++j) h2[j] = fmaf(hv, W2[i][j], h2[j]);
+    for (int i = 0; i < kFc1Out; ++i) h = fmaf(H[r][i], wc[i], h);
+    h = fmaxf(h + b2, 0.f);
+    const float z0 = sum32(h * c0) + cb0;
+    const float z1 = sum32(h * c1) + cb1;
+    const float z2 = sum32(h * c2) + cb2;
+    const float q = sum32(h * mw) + mb;
+    if (j == 0) {
+      const float zm = fmaxf(z0, fmaxf(z1, z2));
+      const float e0 = expf(z0 - zm), e1 = expf(z1 - zm), e2 = expf(z2 - zm);
+      const float inv = 1.f / (e0 + e1 + e2);
+      const float eq = expf(-fabsf(q));
+      const float sig = (q >= 0.f) ? 1.f / (1.f + eq) : eq / (1.f + eq);
+      reinterpret_cast<float4*>(scores)[p0 + r] = make_float4(e0 * inv, e1 * inv, e2 * inv, sig);
+    }
   }
-  float z0 = w.cls_b[0], z1 = w.cls_b[1], z2 = w.cls_b[2], q = w.mic_b[0];
-#pragma unroll
-  for (int j = 0; j < kFc2Out; ++j) {
-    const float v = fmaxf(h2[j] + B2[j], 0.f);
-    z0 = fmaf(v, Hd[j][0], z0);
-    z1 = fmaf(v, Hd[j][1], z1);
-    z2 = fmaf(v, Hd[j][2], z2);
-    q = fmaf(v, Hd[j][3], q);
-  }
-  const float zm = fmaxf(z0, fmaxf(z1, z2));
-  const float e0 = expf(z0 - zm), e1 = expf(z1 - zm), e2 = expf(z2 - zm);
-  const float inv = 1.f / (e0 + e1 + e2);
-  const float eq = expf(-fabsf(q));
-  const float sig = (q >= 0.f) ? 1.f / (1.f + eq) : eq / (1.f + eq);
-  reinterpret_cast<float4*>(scores)[p0 + tid] = make_float4(e0 * inv, e1 * inv, e2 * inv, sig);
 }
 
 }  // namespace
@@ -78,7 +101,7 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
                        float* scores, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   const int64_t blocks = (n + kRows - 1) / kRows;
-  tail_kernel<<<dim3((unsigned)blocks), dim3(64), 0, stream>>>(part, splits, n, w, scores);
+  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, scores);
   return hipGetLastError();
 }
 
