@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run 3 device-to-device copies of MIB MiB (a plain copy kernel of "
+                         "known size, to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -199,6 +202,14 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy << 20, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration: 3 copies of {args.calibrate_copy} MiB")
+        del src, dst
     log(f"[bench] building config {args.config} workload")
     step, n, desc, sample, footprint, hit_bytes = make_workload(args, torch, pid)
     h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)
