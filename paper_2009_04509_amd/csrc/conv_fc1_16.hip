@@ -12,12 +12,14 @@
 // the XCD's 4 MB L2.  Positions are taken in pairs (x, x+1) with x even: the
 // 5x6 pixel window of a pair (30 values) fits one K=32 MFMA operand, shared by
 // both positions.  The block's 8 waves (2 per SIMD, so one wave's conversions
-// overlap the other's MFMAs) form 4 position groups x 2 output halves: the two
-// waves of a group take the same interleaved pairs and the same 96 patches, and
-// each accumulates 64 of the 128 outputs (4 x 6 tiles of 16x16).  Both compute
-// the conv of their pair; each FC1 weight fragment fetched from L2 feeds 6
-// MFMAs and no weight goes through LDS.  LDS holds a ring of 8 patch rows (the 5
-// rows a map row needs, plus the next) for the block's 96 patches.
+// overlap the other's MFMAs) form 4 position groups x 2 output halves.  The two
+// waves of a group take the same interleaved pairs; each computes the conv of
+// half of the 96 patches, and the pair swaps the converted 16-bit fragments
+// through LDS (double-buffered, one block barrier per K-step), so the conv is
+// computed once and each wave streams only the FC1 weights of its 64 outputs:
+// every weight fragment fetched through L1 feeds 6 MFMAs.  LDS also holds a
+// ring of 8 patch rows (the 5 rows a map row needs, plus those prefetched two
+// steps ahead) for the block's 96 patches, and the conv filter fragments.
 //
 // Per pair and per 16-patch tile, v_mfma_f32_16x16x32_{bf16,f16}:
 //   conv:  D[ch][patch] = sum_slot Kc[ch][slot] * Win[slot][patch]
@@ -47,13 +49,21 @@ constexpr int kWaves = kKGroups * kNHalves;   // 8
 constexpr int kThreads = kWaves * 64;         // 512
 constexpr int kMT = 8 / kNHalves;             // 16-output tiles per wave
 constexpr int kBt = 96;                       // patches per block
-constexpr int kTiles = kBt / 16;              // 16-patch MFMA tiles
+constexpr int kTiles = kBt / 16;              // 16-patch MFMA tiles per block
+constexpr int kOwn = kTiles / kNHalves;       // tiles whose conv a wave computes
 constexpr int kPairsPerRow = kFm / 2;         // 22
 constexpr int kRing = 8;                      // patch-row ring slots
 constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
 constexpr int kSlot = kBt * kRP;              // dwords per ring slot
-constexpr int kRegion = kMT * kTiles * 4 * 64;          // one wave's partial sums (floats)
-constexpr int kLdsDwords = (kRing * kSlot > 4 * kRegion) ? kRing * kSlot : 4 * kRegion;
+// LDS layout (dwords): ring | conv filter fragments | swap buffers; the final
+// reduction reuses it from the start.
+constexpr int kConvOff = kRing * kSlot;                         // 19,968
+constexpr int kSwapOff = kConvOff + 6 * 64 * 4;                 // 21,504
+constexpr int kSwapWave = kOwn * 64 * 4;                        // one wave's fragments
+constexpr int kSwapBuf = kWaves * kSwapWave;                    // one buffer
+constexpr int kRegion = kMT * kTiles * 4 * 64;                  // one wave's partial sums
+constexpr int kMain = kSwapOff + 2 * kSwapBuf;                  // 33,792
+constexpr int kLdsDwords = (kMain > 4 * kRegion) ? kMain : 4 * kRegion;
 
 // One patch row (96 B) of each of the block's patches: kBt x 6 chunks of 16 B.
 // Chunk c = tid, plus c = kThreads + tid for the first kRowExtra threads (whole
@@ -102,7 +112,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = wave % kKGroups;            // position group
-  const int nh = wave / kKGroups;            // output half
+  const int nh = wave / kKGroups;            // output half; also the half of the tiles it convolves
+  const int partner = kg + kKGroups * (1 - nh);
   const bool extra = wave < kRowExtra / 64;  // wave-uniform
   const int col = lane & 15;                 // MFMA column (patch within tile) / row
   const int grp = lane >> 4;                 // MFMA K-slot group
@@ -113,13 +124,13 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   const int G0 = (kGroups * split) / kSplits;
   const int steps = (kGroups * (split + 1)) / kSplits - G0;
   const int P0 = kKGroups * G0;
+  using Op = Op16<kFp16>;
 
-  // conv filter fragments: [shift][channel tile]
-  uint4 cw[2][3];
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int t = 0; t < 3; ++t) cw[s][t] = convp[(s * 3 + t) * 64 + lane];
+  // conv filter fragments [shift][channel tile] in LDS; a K-step reads two
+  uint4* cwl = reinterpret_cast<uint4*>(lds + kConvOff);
+  for (int i = tid; i < 6 * 64; i += kThreads) cwl[i] = convp[i];
+  // swap buffers: [buffer][wave][own tile][lane] x 16 B
+  uint4* swp = reinterpret_cast<uint4*>(lds + kSwapOff);
 
   // this lane's 4 window dwords: slot pair f = 8*grp + 2d -> pixel (u, c)
   int woff[4], wrow[4];
@@ -128,22 +139,30 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     int f = 8 * grp + 2 * d;
     if (f > 28) f = 28;                      // slots 30-31 are constants (masked below)
     wrow[d] = f / 6;
-    woff[d] = (f % 6) / 2 + col * kRP;
+    woff[d] = (f % 6) / 2 + col * kRP + nh * kOwn * 16 * kRP;
   }
   const bool const_slot = (grp == 3);
-  using Op = Op16<kFp16>;
 
-  floatx4 acc[kMT][kTiles];
+  // accumulators for the wave's own conv tiles (block tiles nh*kOwn + i) and
+  // for the partner's (tiles (1-nh)*kOwn + i); indexed statically only, so
+  // they stay in registers
+  floatx4 acc_own[kMT][kOwn], acc_oth[kMT][kOwn];
 #pragma unroll
   for (int m = 0; m < kMT; ++m)
 #pragma unroll
-    for (int i = 0; i < kTiles; ++i) acc[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < kOwn; ++i) {
+      acc_own[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
+      acc_oth[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
+    }
 
-  // ---- initial patch rows
-  auto top_row = [&](int step) {             // highest input row needed by a step
-    return (P0 + kKGroups * step + kKGroups - 1) / kPairsPerRow + kK - 1;
+  // ---- patch rows.  The ring is filled two steps ahead of the step being
+  // computed, so the window of step s+1 can be read during step s.
+  auto top_row = [&](int step) {             // highest input row a step needs
+    int pl = P0 + kKGroups * step + kKGroups - 1;
+    if (pl > kPos / 2 - 1) pl = kPos / 2 - 1;
+    return pl / kPairsPerRow + kK - 1;
   };
-  int loaded_hi = top_row(0);
+  int loaded_hi = top_row(1);
   for (int r = P0 / kPairsPerRow; r <= loaded_hi; ++r) {
     uint4 v[2];
     row_load(patches, n, p_base, r, extra, v);
@@ -151,105 +170,181 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   }
   __syncthreads();
 
-  // FC1 fragments through a buffer resource: the fragment base is a scalar
-  // offset and the output tiles are immediate offsets, so the loads need no
-  // per-lane address arithmetic; reads past the end return 0.
+  auto read_win = [&](int P, uint4 (&win)[kOwn]) {
+    const int y = P / kPairsPerRow;
+    const int xh = P - y * kPairsPerRow;     // x / 2
+    int base[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) base[d] = ((y + wrow[d]) & (kRing - 1)) * kSlot + woff[d] + xh;
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) {
+      const int o = i * 16 * kRP;
+      win[i].x = lds[base[0] + o];
+      win[i].y = lds[base[1] + o];
+      win[i].z = lds[base[2] + o];
+      const uint32_t w3 = lds[base[3] + o];
+      win[i].w = const_slot ? Op::kOnes : w3;
+    }
+  };
+  // conv of K-step q (conv tiles (shift, channel tile) feeding it): 2 MFMAs per tile
+  auto conv = [&](int q, const uint4 (&win)[kOwn], floatx4 (&ca)[kOwn], floatx4 (&cb)[kOwn]) {
+    const int sa = (q == 2) ? 1 : 0, ta = (q == 0) ? 0 : (q == 1 ? 2 : 1);
+    const int sb = (q == 0) ? 0 : 1, tb = (q == 0) ? 1 : (q == 1 ? 0 : 2);
+    const uint4 fa = cwl[(sa * 3 + ta) * 64 + lane];
+    const uint4 fb = cwl[(sb * 3 + tb) * 64 + lane];
+    const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) {
+      ca[i] = Op::mfma(fa, win[i], z);
+      cb[i] = Op::mfma(fb, win[i], z);
+    }
+  };
+  // ReLU + round to 16 bits: the conv tiles become FC1 B operands
+  auto convert = [&](const floatx4 (&ca)[kOwn], const floatx4 (&cb)[kOwn], uint4 (&bf)[kOwn]) {
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i)
+      bf[i] = make_uint4(relu2(Op::pack(ca[i][0], ca[i][1])), relu2(Op::pack(ca[i][2], ca[i][3])),
+                         relu2(Op::pack(cb[i][0], cb[i][1])), relu2(Op::pack(cb[i][2], cb[i][3])));
+  };
+  auto put_swap = [&](int buf, const uint4 (&bf)[kOwn]) {
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) swp[((buf * kWaves + wave) * kOwn + i) * 64 + lane] = bf[i];
+  };
+  auto get_swap = [&](int buf, uint4 (&bf)[kOwn]) {
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) bf[i] = swp[((buf * kWaves + partner) * kOwn + i) * 64 + lane];
+  };
+
+  // FC1 fragments of this wave's outputs through a buffer resource: the
+  // fragment base is a scalar offset and the output tiles are immediate
+  // offsets, so the loads need no per-lane address arithmetic; reads past the
+  // end return 0.
   const __amdgpu_buffer_rsrc_t w1r = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint4*>(w1p), (short)0, (int)(kFc1Frags * 16), 0x00020000);
   const int voff = lane * 16 + nh * kMT * 1024;
-  auto load_w = [&](int P, int q, uint4 (&w)[kMT]) {
-    const int so = (P * 3 + q) * 8 * 1024;
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-      w[m] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(w1r, voff + m * 1024, so, 0));
+  auto load_one = [&](int P, int q, int m) {
+    return __builtin_bit_cast(
+        uint4, __builtin_amdgcn_raw_buffer_load_b128(w1r, voff + m * 1024, (P * 3 + q) * 8 * 1024, 0));
   };
-  uint4 wcur[kMT];
-  load_w(P0 + kg, 0, wcur);
+
+  // ---- software pipeline.  Entering a K-step, this wave's own conv fragments
+  // are in registers and the partner's are in swap buffer `buf` (published by
+  // the last barrier).  While the FC1 MFMAs run, the conv of the next K-step is
+  // issued, converted and published in the other buffer.  The FC1 weights sit
+  // in a ring of 3 register sets, one per K-step of a pair (set q for K-step
+  // q), each loaded two K-steps before it is used.
+  uint4 w[3][kMT], win[kOwn], own[kOwn];
+#pragma unroll
+  for (int m = 0; m < kMT; ++m) {
+    w[0][m] = load_one(P0 + kg, 0, m);
+    w[1][m] = load_one(P0 + kg, 1, m);
+  }
+  read_win(P0 + kg, win);
+  {
+    floatx4 ca[kOwn], cb[kOwn];
+    conv(0, win, ca, cb);
+    convert(ca, cb, own);
+  }
+  int buf = 0;
+  put_swap(buf, own);
+  __syncthreads();
 
 #pragma unroll 1
   for (int step = 0; step < steps; ++step) {
-    // prefetch the patch row the next step adds (at most one; block-uniform)
+    // the patch row two steps ahead (at most one per step; block-uniform)
     uint4 rv[2];
-    const int next_hi = (step + 1 < steps) ? top_row(step + 1) : loaded_hi;
-    const bool new_row = next_hi > loaded_hi;
-    if (new_row) row_load(patches, n, p_base, next_hi, extra, rv);
+    const int want_hi = top_row(step + 2);
+    const bool new_row = want_hi > loaded_hi;
+    if (new_row) row_load(patches, n, p_base, want_hi, extra, rv);
 
     const int P = P0 + kKGroups * step + kg;
-    const int y = P / kPairsPerRow;
-    const int xh = P - y * kPairsPerRow;     // x / 2
-    uint4 win[kTiles];
-    {
-      int base[4];
-#pragma unroll
-      for (int d = 0; d < 4; ++d) base[d] = ((y + wrow[d]) & (kRing - 1)) * kSlot + woff[d] + xh;
-#pragma unroll
-      for (int i = 0; i < kTiles; ++i) {
-        const int o = i * 16 * kRP;
-        win[i].x = lds[base[0] + o];
-        win[i].y = lds[base[1] + o];
-        win[i].z = lds[base[2] + o];
-        const uint32_t w3 = lds[base[3] + o];
-        win[i].w = const_slot ? Op::kOnes : w3;
-      }
-    }
+    uint4 win_next[kOwn];
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
-      // prefetch the next FC1 weight step of this wave (past the end reads 0)
-      const int Pn = (q < 2) ? P : P + kKGroups;
-      const int qn = (q < 2) ? q + 1 : 0;
-      uint4 wnext[kMT];
-      load_w(Pn, qn, wnext);
-      // keep these loads here: the scheduler would otherwise sink them to their
-      // use in the next step and expose the full memory latency
-      __builtin_amdgcn_sched_barrier(0);
-      // conv tiles feeding this K=32 step: (shift, channel tile)
-      const int sa = (q == 2) ? 1 : 0, ta = (q == 0) ? 0 : (q == 1 ? 2 : 1);
-      const int sb = (q == 0) ? 0 : 1, tb = (q == 0) ? 1 : (q == 1 ? 0 : 2);
+      const int nq = (q + 1) % 3;            // the next K-step
+      const int fq = (q + 2) % 3;            // the K-step after it
+      const int fP = (q < 1) ? P : P + kKGroups;
+      uint4 oth[kOwn];
+      get_swap(buf, oth);
+      floatx4 ca[kOwn], cb[kOwn];
+      uint4 nxt[kOwn];
+      // own tiles first, while the partner's fragments arrive from LDS
 #pragma unroll
-      for (int i = 0; i < kTiles; ++i) {
-        const floatx4 z = {0.f, 0.f, 0.f, 0.f};
-        const floatx4 ca = Op::mfma(cw[sa][ta], win[i], z);
-        const floatx4 cb = Op::mfma(cw[sb][tb], win[i], z);
-        const uint4 bf = make_uint4(relu2(Op::pack(ca[0], ca[1])), relu2(Op::pack(ca[2], ca[3])),
-                                    relu2(Op::pack(cb[0], cb[1])), relu2(Op::pack(cb[2], cb[3])));
+      for (int m = 0; m < kMT; ++m) {
 #pragma unroll
-        for (int m = 0; m < kMT; ++m) acc[m][i] = Op::mfma(wcur[m], bf, acc[m][i]);
+        for (int i = 0; i < kOwn; ++i) acc_own[m][i] = Op::mfma(w[q][m], own[i], acc_own[m][i]);
+        // past the end of the weights this reads 0
+        w[fq][m] = load_one(fP, fq, m);
+        if (m == 1) {
+          if (q == 1) read_win(P + kKGroups, win_next);
+          if (q == 2)
+            conv(nq, win_next, ca, cb);
+          else
+            conv(nq, win, ca, cb);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
-      for (int m = 0; m < kMT; ++m) wcur[m] = wnext[m];
-    }
-    // The ring slot a new row overwrites held row next_hi - 8, which is below
-    // every row the steps since the last barrier read, so waves may drift
-    // apart between row loads; the barrier publishes the new row before any
-    // wave's next step reads it.  (new_row is block-uniform.)
-    if (new_row) {
-      row_store(lds, next_hi, extra, rv);
-      loaded_hi = next_hi;
+      for (int m = 0; m < kMT; ++m) {
+#pragma unroll
+        for (int i = 0; i < kOwn; ++i)
+          acc_oth[m][i] = Op::mfma(w[q][m], oth[i], acc_oth[m][i]);
+        if (m == 1) {
+          convert(ca, cb, nxt);
+          put_swap(buf ^ 1, nxt);
+        }
+        // fix the interleaving: left alone the scheduler sinks the loads to
+        // their use and bunches the conversions
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int i = 0; i < kOwn; ++i) own[i] = nxt[i];
+      if (q == 2) {
+#pragma unroll
+        for (int i = 0; i < kOwn; ++i) win[i] = win_next[i];
+        // The slot a new row overwrites held a row below every row that any
+        // wave still reads; the barrier below publishes it before the step
+        // that first needs it (two steps later).
+        if (new_row) {
+          row_store(lds, want_hi, extra, rv);
+          loaded_hi = want_hi;
+        }
+      }
+      buf ^= 1;
+      // publishes the next K-step's swap fragments (and a new row); the
+      // buffer written next was last read before this barrier
       __syncthreads();
     }
   }
-  __syncthreads();
 
   // ---- fixed-order reduction over position groups, per output half:
   //      (g0 + g2) + (g1 + g3)
   float* red = reinterpret_cast<float*>(lds);
+  // (all waves of one output half share the own/partner tile order)
+  auto slot = [&](int region, int m, int i, int e) {
+    return region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane;
+  };
   auto put = [&](int region) {
 #pragma unroll
     for (int m = 0; m < kMT; ++m)
 #pragma unroll
-      for (int i = 0; i < kTiles; ++i)
+      for (int i = 0; i < kOwn; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          red[region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane] = acc[m][i][e];
+        for (int e = 0; e < 4; ++e) {
+          red[slot(region, m, i, e)] = acc_own[m][i][e];
+          red[slot(region, m, kOwn + i, e)] = acc_oth[m][i][e];
+        }
   };
   auto add = [&](int region) {
 #pragma unroll
     for (int m = 0; m < kMT; ++m)
 #pragma unroll
-      for (int i = 0; i < kTiles; ++i)
+      for (int i = 0; i < kOwn; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          acc[m][i][e] += red[region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane];
+        for (int e = 0; e < 4; ++e) {
+          acc_own[m][i][e] += red[slot(region, m, i, e)];
+          acc_oth[m][i][e] += red[slot(region, m, kOwn + i, e)];
+        }
   };
   if (kg >= 2) put(nh * 2 + (kg - 2));
   __syncthreads();
@@ -260,15 +355,19 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   if (kg != 0) return;
   add(nh);
 
-  // acc[m][i]: outputs 16(nh*kMT + m) + 4*grp + e for patch 16i + col
+  // acc_*[m][i]: outputs 16(nh*kMT + m) + 4*grp + e for patch 16*tile + col
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
 #pragma unroll
-  for (int i = 0; i < kTiles; ++i) {
-    const int64_t p = (int64_t)i * 16 + col;
-    if (p_base + p < n) {
+  for (int i = 0; i < kOwn; ++i) {
+    const int64_t po = (int64_t)(nh * kOwn + i) * 16 + col;
+    const int64_t pp = (int64_t)((1 - nh) * kOwn + i) * 16 + col;
+    // the partials are read once, by the tail kernel: non-temporal stores keep
+    // them from evicting the FC1 weight slices from L2
 #pragma unroll
-      for (int m = 0; m < kMT; ++m)
-        *reinterpret_cast<floatx4*>(dst + p * kFc1Out + 16 * (nh * kMT + m) + 4 * grp) = acc[m][i];
+    for (int m = 0; m < kMT; ++m) {
+      const int o = 16 * (nh * kMT + m) + 4 * grp;
+      if (p_base + po < n) __builtin_nontemporal_store(acc_own[m][i], reinterpret_cast<floatx4*>(dst + po * kFc1Out + o));
+      if (p_base + pp < n) __builtin_nontemporal_store(acc_oth[m][i], reinterpret_cast<floatx4*>(dst + pp * kFc1Out + o));
     }
   }
 }
