@@ -170,7 +170,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   }
   __syncthreads();
 
-  auto read_win = [&](int P, uint4 (&win)[kOwn]) {
+  // window of pair P; the constant slots are set by fix_win, which the main
+  // loop issues a few MFMAs later so that no VALU op waits on the LDS reads
+  auto read_win_raw = [&](int P, uint4 (&win)[kOwn]) {
     const int y = P / kPairsPerRow;
     const int xh = P - y * kPairsPerRow;     // x / 2
     int base[4];
@@ -182,33 +184,27 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
       win[i].x = lds[base[0] + o];
       win[i].y = lds[base[1] + o];
       win[i].z = lds[base[2] + o];
-      const uint32_t w3 = lds[base[3] + o];
-      win[i].w = const_slot ? Op::kOnes : w3;
+      win[i].w = lds[base[3] + o];
     }
   };
-  // conv of K-step q (conv tiles (shift, channel tile) feeding it): 2 MFMAs per tile
-  auto conv = [&](int q, const uint4 (&win)[kOwn], floatx4 (&ca)[kOwn], floatx4 (&cb)[kOwn]) {
+  auto fix_win = [&](uint4 (&win)[kOwn]) {
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) win[i].w = const_slot ? Op::kOnes : win[i].w;
+  };
+  // filter fragments of K-step q: conv tiles (shift, channel tile) feeding it
+  auto read_filters = [&](int q, uint4& fa, uint4& fb) {
     const int sa = (q == 2) ? 1 : 0, ta = (q == 0) ? 0 : (q == 1 ? 2 : 1);
     const int sb = (q == 0) ? 0 : 1, tb = (q == 0) ? 1 : (q == 1 ? 0 : 2);
-    const uint4 fa = cwl[(sa * 3 + ta) * 64 + lane];
-    const uint4 fb = cwl[(sb * 3 + tb) * 64 + lane];
-    const floatx4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < kOwn; ++i) {
-      ca[i] = Op::mfma(fa, win[i], z);
-      cb[i] = Op::mfma(fb, win[i], z);
-    }
+    fa = cwl[(sa * 3 + ta) * 64 + lane];
+    fb = cwl[(sb * 3 + tb) * 64 + lane];
   };
-  // ReLU + round to 16 bits: the conv tiles become FC1 B operands
-  auto convert = [&](const floatx4 (&ca)[kOwn], const floatx4 (&cb)[kOwn], uint4 (&bf)[kOwn]) {
-#pragma unroll
-    for (int i = 0; i < kOwn; ++i)
-      bf[i] = make_uint4(relu2(Op::pack(ca[i][0], ca[i][1])), relu2(Op::pack(ca[i][2], ca[i][3])),
-                         relu2(Op::pack(cb[i][0], cb[i][1])), relu2(Op::pack(cb[i][2], cb[i][3])));
+  // ReLU + round to 16 bits: a conv tile pair becomes an FC1 B operand
+  auto convert1 = [&](const floatx4& ca, const floatx4& cb) {
+    return make_uint4(relu2(Op::pack(ca[0], ca[1])), relu2(Op::pack(ca[2], ca[3])),
+                      relu2(Op::pack(cb[0], cb[1])), relu2(Op::pack(cb[2], cb[3])));
   };
-  auto put_swap = [&](int buf, const uint4 (&bf)[kOwn]) {
-#pragma unroll
-    for (int i = 0; i < kOwn; ++i) swp[((buf * kWaves + wave) * kOwn + i) * 64 + lane] = bf[i];
+  auto put1 = [&](int buf, int i, const uint4& bf) {
+    swp[((buf * kWaves + wave) * kOwn + i) * 64 + lane] = bf;
   };
   auto get_swap = [&](int buf, uint4 (&bf)[kOwn]) {
 #pragma unroll
@@ -239,14 +235,18 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     w[0][m] = load_one(P0 + kg, 0, m);
     w[1][m] = load_one(P0 + kg, 1, m);
   }
-  read_win(P0 + kg, win);
+  read_win_raw(P0 + kg, win);
+  fix_win(win);
   {
-    floatx4 ca[kOwn], cb[kOwn];
-    conv(0, win, ca, cb);
-    convert(ca, cb, own);
+    uint4 fa, fb;
+    read_filters(0, fa, fb);
+    const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kOwn; ++i) own[i] = convert1(Op::mfma(fa, win[i], z), Op::mfma(fb, win[i], z));
   }
   int buf = 0;
-  put_swap(buf, own);
+#pragma unroll
+  for (int i = 0; i < kOwn; ++i) put1(buf, i, own[i]);
   __syncthreads();
 
 #pragma unroll 1
@@ -264,39 +264,62 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
       const int nq = (q + 1) % 3;            // the next K-step
       const int fq = (q + 2) % 3;            // the K-step after it
       const int fP = (q < 1) ? P : P + kKGroups;
-      uint4 oth[kOwn];
-      get_swap(buf, oth);
+      uint4 oth[kOwn], nxt[kOwn], fa, fb;
       floatx4 ca[kOwn], cb[kOwn];
-      uint4 nxt[kOwn];
-      // own tiles first, while the partner's fragments arrive from LDS
-#pragma unroll
-      for (int m = 0; m < kMT; ++m) {
+      const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+      // One K-step in ten groups of 3 MFMAs, the other work spread between
+      // them: the two waves sharing a SIMD run the same sequence at about the
+      // same time, so neither may bunch its VALU or LDS work.  The weight
+      // register set q is used by groups 0-1, 4-5 (own tiles) and 6-9
+      // (partner's tiles); set fq, last used in the previous K-step, is
+      // reloaded for two K-steps ahead (past the end of the weights this reads 0).
+      auto own_group = [&](int m) {
 #pragma unroll
         for (int i = 0; i < kOwn; ++i) acc_own[m][i] = Op::mfma(w[q][m], own[i], acc_own[m][i]);
-        // past the end of the weights this reads 0
-        w[fq][m] = load_one(fP, fq, m);
-        if (m == 1) {
-          if (q == 1) read_win(P + kKGroups, win_next);
-          if (q == 2)
-            conv(nq, win_next, ca, cb);
-          else
-            conv(nq, win, ca, cb);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      };
+      auto oth_group = [&](int m) {
 #pragma unroll
-      for (int m = 0; m < kMT; ++m) {
+        for (int i = 0; i < kOwn; ++i) acc_oth[m][i] = Op::mfma(w[q][m], oth[i], acc_oth[m][i]);
+      };
+      // g0: next filters, then the partner's fragments, from LDS (LDS returns
+      // in order, and the filters are needed first)
+      read_filters(nq, fa, fb);
+      get_swap(buf, oth);
+      own_group(0);
+      w[fq][0] = load_one(fP, fq, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      own_group(1);
+      w[fq][1] = load_one(fP, fq, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      // g2, g3: conv of the next K-step
 #pragma unroll
-        for (int i = 0; i < kOwn; ++i)
-          acc_oth[m][i] = Op::mfma(w[q][m], oth[i], acc_oth[m][i]);
-        if (m == 1) {
-          convert(ca, cb, nxt);
-          put_swap(buf ^ 1, nxt);
-        }
-        // fix the interleaving: left alone the scheduler sinks the loads to
-        // their use and bunches the conversions
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      for (int i = 0; i < kOwn; ++i) ca[i] = Op::mfma(fa, (q == 2) ? win_next[i] : win[i], z);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < kOwn; ++i) cb[i] = Op::mfma(fb, (q == 2) ? win_next[i] : win[i], z);
+      __builtin_amdgcn_sched_barrier(0);
+      own_group(2);
+      w[fq][2] = load_one(fP, fq, 2);
+      if (q == 1) read_win_raw(P + kKGroups, win_next);
+      __builtin_amdgcn_sched_barrier(0);
+      own_group(3);
+      w[fq][3] = load_one(fP, fq, 3);
+      nxt[0] = convert1(ca[0], cb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      oth_group(0);
+      nxt[1] = convert1(ca[1], cb[1]);
+      put1(buf ^ 1, 0, nxt[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      oth_group(1);
+      nxt[2] = convert1(ca[2], cb[2]);
+      put1(buf ^ 1, 1, nxt[1]);
+      if (q == 1) fix_win(win_next);
+      __builtin_amdgcn_sched_barrier(0);
+      oth_group(2);
+      put1(buf ^ 1, 2, nxt[2]);
+      __builtin_amdgcn_sched_barrier(0);
+      oth_group(3);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < kOwn; ++i) own[i] = nxt[i];
       if (q == 2) {
