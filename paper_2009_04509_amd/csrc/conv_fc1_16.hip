@@ -53,6 +53,9 @@ constexpr int kTiles = kBt / 16;              // 16-patch MFMA tiles per block
 constexpr int kOwn = kTiles / kNHalves;       // tiles whose conv a wave computes
 constexpr int kPairsPerRow = kFm / 2;         // 22
 constexpr int kRing = 8;                      // patch-row ring slots
+// rows the first two steps of a split need: pairs P0 .. P0 + 2 kKGroups - 1 span
+// at most two map rows, plus the filter height
+constexpr int kPrologueRows = 2 + 5 - 1;
 constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
 constexpr int kSlot = kBt * kRP;              // dwords per ring slot
 // LDS layout (dwords): ring | conv filter fragments | swap buffers; the final
@@ -127,8 +130,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   using Op = Op16<kFp16>;
 
   // conv filter fragments [shift][channel tile] in LDS; a K-step reads two
+  // (copied below, with the first patch rows, so both loads are in flight together)
   uint4* cwl = reinterpret_cast<uint4*>(lds + kConvOff);
-  for (int i = tid; i < 6 * 64; i += kThreads) cwl[i] = convp[i];
+  static_assert(6 * 64 <= kThreads, "one filter chunk per thread");
   // swap buffers: [buffer][wave][own tile][lane] x 16 B
   uint4* swp = reinterpret_cast<uint4*>(lds + kSwapOff);
 
@@ -162,11 +166,19 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     if (pl > kPos / 2 - 1) pl = kPos / 2 - 1;
     return pl / kPairsPerRow + kK - 1;
   };
+  // all rows in flight at once (at most kPrologueRows), then into the ring
   int loaded_hi = top_row(1);
-  for (int r = P0 / kPairsPerRow; r <= loaded_hi; ++r) {
-    uint4 v[2];
-    row_load(patches, n, p_base, r, extra, v);
-    row_store(lds, r, extra, v);
+  {
+    const int r0 = P0 / kPairsPerRow;
+    uint4 v[kPrologueRows][2], fv;
+    if (tid < 6 * 64) fv = convp[tid];
+#pragma unroll
+    for (int j = 0; j < kPrologueRows; ++j)
+      if (r0 + j <= loaded_hi) row_load(patches, n, p_base, r0 + j, extra, v[j]);
+    if (tid < 6 * 64) cwl[tid] = fv;
+#pragma unroll
+    for (int j = 0; j < kPrologueRows; ++j)
+      if (r0 + j <= loaded_hi) row_store(lds, r0 + j, extra, v[j]);
   }
   __syncthreads();
 
@@ -342,32 +354,29 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
 
   // ---- fixed-order reduction over position groups, per output half:
   //      (g0 + g2) + (g1 + g3)
-  float* red = reinterpret_cast<float*>(lds);
+  // one 16 B accumulator tile per lane and access (conflict-free b128)
+  floatx4* red = reinterpret_cast<floatx4*>(lds);
   // (all waves of one output half share the own/partner tile order)
-  auto slot = [&](int region, int m, int i, int e) {
-    return region * kRegion + ((m * kTiles + i) * 4 + e) * 64 + lane;
+  auto slot = [&](int region, int m, int i) {
+    return region * (kRegion / 4) + (m * kTiles + i) * 64 + lane;
   };
   auto put = [&](int region) {
 #pragma unroll
     for (int m = 0; m < kMT; ++m)
 #pragma unroll
-      for (int i = 0; i < kOwn; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          red[slot(region, m, i, e)] = acc_own[m][i][e];
-          red[slot(region, m, kOwn + i, e)] = acc_oth[m][i][e];
-        }
+      for (int i = 0; i < kOwn; ++i) {
+        red[slot(region, m, i)] = acc_own[m][i];
+        red[slot(region, m, kOwn + i)] = acc_oth[m][i];
+      }
   };
   auto add = [&](int region) {
 #pragma unroll
     for (int m = 0; m < kMT; ++m)
 #pragma unroll
-      for (int i = 0; i < kOwn; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc_own[m][i][e] += red[slot(region, m, i, e)];
-          acc_oth[m][i][e] += red[slot(region, m, kOwn + i, e)];
-        }
+      for (int i = 0; i < kOwn; ++i) {
+        acc_own[m][i] += red[slot(region, m, i)];
+        acc_oth[m][i] += red[slot(region, m, kOwn + i)];
+      }
   };
   if (kg >= 2) put(nh * 2 + (kg - 2));
   __syncthreads();

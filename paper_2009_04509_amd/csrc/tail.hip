@@ -1,11 +1,11 @@
 // Split-K reduction of FC1 and the rest of the network (paper §2.2):
-// h1 = ReLU(b1 + sum_s part[s]), h2 = ReLU(b2 + h1 W2), then the softmax
-// branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
+// h1 = ReLU(b1 + sum of the FC1 partial sums), h2 = ReLU(b2 + h1 W2), then the
+// softmax branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
-// A block of 256 threads handles 64 patches.
-//   1. Each thread owns one float4 column slice of 8 patch rows and sums the
-//      partials in ascending split order (coalesced 512 B rows), adds b1,
-//      applies ReLU and stores h1 in LDS.
+// A block of 256 threads handles 96 patches.
+//   1. Each thread owns one float4 column slice of 12 patch rows, adds the
+//      partials of the splits in ascending order (coalesced 512 B rows), adds
+//      b1, applies ReLU and stores h1 in LDS.
 //   2. A group of 32 lanes evaluates one patch at a time: lane j keeps column j
 //      of W2 in registers and forms h2[j] from h1 broadcast out of LDS; the
 //      four head inputs are reduced across the 32 lanes by a fixed butterfly.
@@ -16,13 +16,20 @@
 namespace pointid {
 namespace {
 
-constexpr int kRows = 64;                  // patches per block
+constexpr int kRows = 96;                   // patches per block
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 
 __device__ __forceinline__ float sum32(float v) {
 #pragma unroll
   for (int m = 16; m >= 1; m >>= 1) v += __shfl_xor(v, m, 32);
   return v;
+}
+
+__device__ __forceinline__ void add4(float4& a, const float4& v) {
+  a.x += v.x;
+  a.y += v.y;
+  a.z += v.z;
+  a.w += v.w;
 }
 
 __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
@@ -44,13 +51,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
 #pragma unroll
       for (int k = 0; k < kRows / 8; ++k) {
         const int r = r0 + 8 * k;
-        if (p0 + r < n) {
-          const float4 v = src[r * (kFc1Out / 4) + c4];
-          acc[k].x += v.x;
-          acc[k].y += v.y;
-          acc[k].z += v.z;
-          acc[k].w += v.w;
-        }
+        if (p0 + r < n) add4(acc[k], src[r * (kFc1Out / 4) + c4]);
       }
     }
     const float4 b = reinterpret_cast<const float4*>(w.fc1_b)[c4];
@@ -100,6 +101,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
 hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWeights& w,
                        float* scores, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
+  if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
   tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, scores);
   return hipGetLastError();
