@@ -2,13 +2,15 @@
 // h1 = ReLU(b1 + sum of the FC1 partial sums), h2 = ReLU(b2 + h1 W2), then the
 // softmax branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
-// A block of 256 threads handles 96 patches.
-//   1. Each thread owns one float4 column slice of 12 patch rows, adds the
-//      partials of the splits in ascending order (coalesced 512 B rows), adds
-//      b1, applies ReLU and stores h1 in LDS.
+// A block of 256 threads handles 32 patches.
+//   1. Each thread owns one float4 column slice of 4 patch rows; it issues the
+//      loads of all the splits' partials at once (coalesced 512 B rows), then
+//      adds them in ascending split order, adds b1, applies ReLU and stores h1
+//      in LDS.
 //   2. A group of 32 lanes evaluates one patch at a time: lane j keeps column j
-//      of W2 in registers and forms h2[j] from h1 broadcast out of LDS; the
-//      four head inputs are reduced across the 32 lanes by a fixed butterfly.
+//      of W2 in registers (staged once per block through LDS) and forms h2[j]
+//      from h1 broadcast out of LDS; the four head inputs are reduced across
+//      the 32 lanes by a fixed butterfly.
 // Every patch is computed by the same instruction sequence whatever its
 // position, so results do not depend on the batch or the hit order.
 #include "internal.h"
@@ -16,7 +18,8 @@
 namespace pointid {
 namespace {
 
-constexpr int kRows = 96;                   // patches per block
+constexpr int kRows = 32;                   // patches per block
+constexpr int kMaxSplits = 8;               // splits whose loads are in flight together
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 
 __device__ __forceinline__ float sum32(float v) {
@@ -36,8 +39,12 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
                                                    int64_t n, DeviceWeights w,
                                                    float* __restrict__ scores) {
   __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
+  __shared__ __attribute__((aligned(16))) float W2s[kFc1Out * kFc2Out];
   const int tid = threadIdx.x;
   const int64_t p0 = (int64_t)blockIdx.x * kRows;
+  // W2 (16 KiB) into LDS: 4 float4 per thread, coalesced
+  for (int i = tid; i < kFc1Out * kFc2Out / 4; i += 256)
+    reinterpret_cast<float4*>(W2s)[i] = reinterpret_cast<const float4*>(w.fc2_w)[i];
 
   // ---- 1. fixed-order split-K reduction, + b1, ReLU
   {
@@ -46,13 +53,23 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
     float4 acc[kRows / 8];
 #pragma unroll
     for (int k = 0; k < kRows / 8; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < splits; ++s) {
-      const float4* src = reinterpret_cast<const float4*>(part + ((int64_t)s * n + p0) * kFc1Out);
+    for (int s0 = 0; s0 < splits; s0 += kMaxSplits) {
+      float4 v[kMaxSplits][kRows / 8];
 #pragma unroll
-      for (int k = 0; k < kRows / 8; ++k) {
-        const int r = r0 + 8 * k;
-        if (p0 + r < n) add4(acc[k], src[r * (kFc1Out / 4) + c4]);
+      for (int s = 0; s < kMaxSplits; ++s) {
+        const float4* src =
+            reinterpret_cast<const float4*>(part + ((int64_t)(s0 + s) * n + p0) * kFc1Out);
+#pragma unroll
+        for (int k = 0; k < kRows / 8; ++k) {
+          const int r = r0 + 8 * k;
+          v[s][k] = (s0 + s < splits && p0 + r < n) ? src[r * (kFc1Out / 4) + c4]
+                                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
       }
+#pragma unroll
+      for (int s = 0; s < kMaxSplits; ++s)
+#pragma unroll
+        for (int k = 0; k < kRows / 8; ++k) add4(acc[k], v[s][k]);
     }
     const float4 b = reinterpret_cast<const float4*>(w.fc1_b)[c4];
 #pragma unroll
@@ -70,7 +87,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
   const int grp = tid >> 5;                  // 8 groups
   float wc[kFc1Out];
 #pragma unroll
-  for (int i = 0; i < kFc1Out; ++i) wc[i] = w.fc2_w[i * kFc2Out + j];
+  for (int i = 0; i < kFc1Out; ++i) wc[i] = W2s[i * kFc2Out + j];
   const float b2 = w.fc2_b[j];
   const float c0 = w.cls_w[j * 3 + 0], c1 = w.cls_w[j * 3 + 1], c2 = w.cls_w[j * 3 + 2];
   const float mw = w.mic_w[j];
