@@ -59,9 +59,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4])
+    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
     ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
+    ap.add_argument("--streams", type=int, default=64, help="config 5: request streams")
+    ap.add_argument("--per-stream", type=int, default=32, help="config 5: requests per stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -190,6 +192,84 @@ def cpu_baseline(sample, n_sample):
             "sample": f"{what}; {dt:.1f} s", "seconds": round(dt, 2)}
 
 
+def serving(args, torch, pid, synth):
+    """Config 5: 8 resident config-2 planes; requests of 1,000-8,000 hits sent on
+    `--streams` streams, `--per-stream` each, enqueued round-robin.  One step
+    classifies every request; the value is hits per second of wall-clock time
+    from the first enqueue to the completion of the last request (host enqueue
+    cost included).  Per-request latency is the time between events recorded on
+    the request's stream just before and just after its call."""
+    dev = "cuda:0"
+    planes, reqs = synth.config5_requests(n_planes=8, n_streams=args.streams,
+                                          per_stream=args.per_stream)
+    imgs = [torch.from_numpy(p.image).to(dev) for p in planes]
+    hits = [[torch.from_numpy(x).to(dev) for (_, x) in rs] for rs in reqs]
+    outs = [[torch.empty((len(x), 4), dtype=torch.float32, device=dev) for (_, x) in rs]
+            for rs in reqs]
+    streams = [torch.cuda.Stream() for _ in reqs]
+    total = sum(len(x) for rs in reqs for (_, x) in rs)
+    h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)
+
+    def one_step():
+        evs = []
+        for k in range(args.per_stream):
+            for s, rs in enumerate(reqs):
+                st = streams[s]
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(st)
+                pid.pointid_classify(h, imgs[rs[k][0]], hits[s][k], outs[s][k], stream=st)
+                e1.record(st)
+                evs.append((e0, e1))
+        return evs
+
+    log(f"[bench] serving: {args.streams} streams x {args.per_stream} requests, {total} hits; "
+        f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    pid.pointid_timing_reset()
+    pid.pointid_timing_enable(True)
+    lat, walls = [], []
+    for _ in range(args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        evs = one_step()
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t0)
+        lat += [a.elapsed_time(b) for a, b in evs]
+    pid.pointid_timing_enable(False)
+    wall = float(np.sum(walls))
+    value = total * args.steps / wall
+    lat = np.asarray(lat)
+    log(f"[bench] {args.steps} steps: {wall / args.steps * 1e3:.2f} ms/step, "
+        f"{value / 1e6:.2f} M patches/s; latency p50 {np.percentile(lat, 50):.3f} ms "
+        f"p99 {np.percentile(lat, 99):.3f} ms")
+    kern = {}
+    for name in KERNELS:
+        tot, cnt = pid.pointid_timing_query(name)
+        if cnt:
+            kern[name] = {"ms_per_step": round(tot / args.steps, 4), "launches": cnt,
+                          "avg_launch_ms": round(tot / cnt, 4)}
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": args.precision, "data": "synthetic",
+        "config": {"workload": f"serving: 8 resident planes (480 wires x 6000 ticks), "
+                               f"{args.streams} streams x {args.per_stream} requests of "
+                               f"1,000-8,000 hits, one pointid_classify per request",
+                   "hits": total, "requests": args.streams * args.per_stream,
+                   "precision": args.precision},
+        "latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
+                       "p99": round(float(np.percentile(lat, 99)), 4),
+                       "mean": round(float(lat.mean()), 4)},
+        "kernels": kern,
+    }
+    h.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -210,6 +290,9 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] calibration: 3 copies of {args.calibrate_copy} MiB")
         del src, dst
+    if args.config == 5:
+        serving(args, torch, pid, synth)
+        return
     log(f"[bench] building config {args.config} workload")
     step, n, desc, sample, footprint, hit_bytes = make_workload(args, torch, pid)
     h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)

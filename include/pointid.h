@@ -23,8 +23,11 @@
  *     stream has passed the call.  Weight pointers are HOST pointers.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Calls
  *     only enqueue work on it; none synchronises the host.  Temporary device
- *     memory is taken from the device's stream-ordered pool on `stream` and
- *     returned to it on `stream`.
+ *     memory comes from scratch buffers the handle caches until
+ *     pointid_destroy: a call takes a free buffer that its stream last used or
+ *     whose last use has finished (else it makes `stream` wait for that use),
+ *     so calls after the first few allocate nothing; a call allocates
+ *     (hipMalloc) only when no cached buffer is free and big enough.
  *   - A handle is immutable after pointid_create: any number of host threads
  *     and streams may use one handle at once.
  *   - Results are deterministic: identical inputs give identical bits, and

@@ -1,5 +1,5 @@
 // C ABI of libpointid (declared in include/pointid.h): argument validation,
-// weight upload, workspace from the stream-ordered pool, launch sequencing.
+// weight upload, device scratch from a per-handle cache, launch sequencing.
 // Every call only enqueues work on the caller's stream.
 #include "pointid.h"
 
@@ -15,11 +15,31 @@
 
 using namespace pointid;
 
+// Per-handle cache of device scratch buffers, reused across calls.  A call
+// takes one buffer big enough for all its scratch and records an event on its
+// stream after enqueueing its work; the next user of the buffer either runs on
+// the same stream (stream order protects it) or finds that event complete, and
+// only when neither is possible waits for it on its own stream.  Buffers are
+// allocated only when no free one fits, so steady-state calls allocate nothing.
+struct ScratchPool {
+  struct Entry {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    hipEvent_t done = nullptr;     // recorded after the last user's work
+    hipStream_t last = nullptr;    // stream of the last user
+    bool used = false;             // `done` has been recorded
+    bool busy = false;             // taken by a call being enqueued
+  };
+  std::mutex mu;
+  std::vector<Entry> entries;
+};
+
 struct pointid_s {
   int device;
   int precision;
   DeviceWeights w;     // device pointers into `blob`
   void* blob;          // one allocation holding every parameter tensor
+  ScratchPool* scratch;
 };
 
 namespace {
@@ -103,29 +123,118 @@ class KernelTimer {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-// Stream-ordered scratch: allocated on `stream`, freed on `stream` when the
-// scope ends (after the work enqueued in between).
+constexpr size_t kScratchAlign = 256;
+constexpr size_t kMaxScratchBuffers = 512;
+size_t pad256(size_t b) { return (b + kScratchAlign - 1) / kScratchAlign * kScratchAlign; }
+
+// One call's scratch: a buffer of the handle's ScratchPool, handed back (with
+// its event recorded on the call's stream) when the scope ends.
 class Workspace {
  public:
-  explicit Workspace(hipStream_t s) : s_(s) {}
+  Workspace(ScratchPool* pool, hipStream_t s) : pool_(pool), s_(s) {}
   ~Workspace() {
-    for (void* p : ptrs_) (void)hipFreeAsync(p, s_);
+    if (idx_ < 0) return;
+    hipError_t e = hipEventRecord(done_, s_);
+    // without the event, the next user could not tell when this call's work
+    // is done: wait for it here (an error path only)
+    if (e != hipSuccess) (void)hipStreamSynchronize(s_);
+    std::lock_guard<std::mutex> g(pool_->mu);
+    ScratchPool::Entry& en = pool_->entries[idx_];
+    en.busy = false;
+    en.last = s_;
+    en.used = (e == hipSuccess);
   }
+
+  // Takes a buffer of at least `bytes` for this call.
+  hipError_t reserve(size_t bytes) {
+    std::unique_lock<std::mutex> g(pool_->mu);
+    std::vector<ScratchPool::Entry>& v = pool_->entries;
+    int same = -1, ready = -1, any = -1;
+    for (int i = 0; i < (int)v.size(); ++i) {
+      const ScratchPool::Entry& en = v[i];
+      if (en.busy || en.bytes < bytes) continue;
+      if (en.last == s_ || !en.used) {
+        if (same < 0 || en.bytes < v[same].bytes) same = i;
+      } else if (hipEventQuery(en.done) == hipSuccess) {
+        if (ready < 0 || en.bytes < v[ready].bytes) ready = i;
+      } else if (any < 0 || en.bytes < v[any].bytes) {
+        any = i;
+      }
+    }
+    int pick = same >= 0 ? same : ready;
+    if (pick < 0 && (v.size() >= kMaxScratchBuffers)) pick = any;
+    if (pick >= 0) {
+      take(pick);
+      const bool wait = v[pick].used && v[pick].last != s_ && pick != ready;
+      g.unlock();
+      return wait ? hipStreamWaitEvent(s_, done_, 0) : hipSuccess;
+    }
+    // a new buffer, sized to the next power of two (at least 4 MiB) so that
+    // requests of varying size share buffers
+    v.emplace_back();
+    const int slot = (int)v.size() - 1;
+    v[slot].busy = true;
+    g.unlock();
+    size_t cap = size_t(4) << 20;
+    while (cap < bytes) cap <<= 1;
+    void* p = nullptr;
+    hipEvent_t ev = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipMalloc(&p, cap);
+    g.lock();
+    if (e != hipSuccess) {
+      if (ev) (void)hipEventDestroy(ev);
+      v[slot] = ScratchPool::Entry();            // empty, free: skipped by later calls
+      return e;
+    }
+    v[slot].ptr = p;
+    v[slot].bytes = cap;
+    v[slot].done = ev;
+    take(slot);
+    return hipSuccess;
+  }
+
+  // Carves the next piece (256-byte aligned) out of the reserved buffer.
   hipError_t get(size_t bytes, void** out) {
     *out = nullptr;
     if (bytes == 0) return hipSuccess;
-    hipError_t e = hipMallocAsync(out, bytes, s_);
-    if (e == hipSuccess) ptrs_.push_back(*out);
-    return e;
+    if (idx_ < 0 || used_ + pad256(bytes) > cap_) return hipErrorInvalidValue;
+    *out = base_ + used_;
+    used_ += pad256(bytes);
+    return hipSuccess;
   }
 
  private:
+  void take(int i) {                           // with pool_->mu held
+    ScratchPool::Entry& en = pool_->entries[i];
+    en.busy = true;
+    idx_ = i;
+    base_ = static_cast<char*>(en.ptr);
+    cap_ = en.bytes;
+    done_ = en.done;
+  }
+
+  ScratchPool* pool_;
   hipStream_t s_;
-  std::vector<void*> ptrs_;
+  int idx_ = -1;
+  char* base_ = nullptr;
+  size_t cap_ = 0, used_ = 0;
+  hipEvent_t done_ = nullptr;
 };
 
+// Scratch bytes of one call: 16-bit or fp32 patches (when the call makes
+// them), the FC1 split-K partials and, on the fp32 path, one chunk of maps.
 constexpr int kSplitsFp32 = 8;            // FC1 split-K on the vector fp32 path
 constexpr int64_t kChunkFp32 = 2048;      // patches whose maps are live at once
+size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
+  const bool half = precision != POINTID_FP32;
+  size_t b = 0;
+  if (makes_patches) b += pad256((half ? 2 : 4) * (size_t)n * kPatchPix);
+  const int S = half ? conv_fc1_16_splits() : kSplitsFp32;
+  b += pad256(sizeof(float) * (size_t)S * n * kFc1Out);
+  if (!half) b += pad256(sizeof(float) * (size_t)(n < kChunkFp32 ? n : kChunkFp32) * kFc1In);
+  return b;
+}
 
 // fp32 handles: patches (fp32 [n][2304]) -> scores.
 int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* scores,
@@ -185,10 +294,12 @@ int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hit
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
-  Workspace ws(stream);
+  Workspace ws(h->scratch, stream);
+  hipError_t e = ws.reserve(scratch_bytes(h->precision, n, true));
+  if (e != hipSuccess) return hip_fail(e, "scratch buffer");
   const bool half = h->precision != POINTID_FP32;
   void* patches = nullptr;
-  hipError_t e = ws.get((half ? 2 : 4) * (size_t)n * kPatchPix, &patches);
+  e = ws.get((half ? 2 : 4) * (size_t)n * kPatchPix, &patches);
   if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
   {
     KernelTimer kt("gather", stream);
@@ -290,14 +401,6 @@ int pointid_create(const pointid_weights* w, int precision, int device,
   DeviceScope dev(device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
 
-  // Keep freed stream-ordered workspace cached in the pool instead of
-  // returning it to the OS after every call.
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
-    uint64_t thr = UINT64_MAX;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
-  }
-
   auto* hnd = new (std::nothrow) pointid_s();
   if (!hnd) return fail(POINTID_ENOMEM, "host allocation failed");
   hnd->device = device;
@@ -364,6 +467,12 @@ int pointid_create(const pointid_weights* w, int precision, int device,
       return hip_fail(e, "weight packing");
     }
   }
+  hnd->scratch = new (std::nothrow) ScratchPool();
+  if (!hnd->scratch) {
+    (void)hipFree(hnd->blob);
+    delete hnd;
+    return fail(POINTID_ENOMEM, "host allocation failed");
+  }
   *out = hnd;
   return POINTID_OK;
 }
@@ -374,6 +483,13 @@ int pointid_destroy(pointid_handle h) {
     DeviceScope dev(h->device);
     (void)hipDeviceSynchronize();
     if (h->blob) (void)hipFree(h->blob);
+    if (h->scratch) {
+      for (ScratchPool::Entry& en : h->scratch->entries) {
+        if (en.ptr) (void)hipFree(en.ptr);
+        if (en.done) (void)hipEventDestroy(en.done);
+      }
+      delete h->scratch;
+    }
   }
   delete h;
   return POINTID_OK;
@@ -425,10 +541,12 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
-  Workspace ws(stream);
+  Workspace ws(h->scratch, stream);
+  hipError_t e = ws.reserve(scratch_bytes(h->precision, n, h->precision != POINTID_FP32));
+  if (e != hipSuccess) return hip_fail(e, "scratch buffer");
   if (h->precision == POINTID_FP32) return run_network_fp32(h, patches, n, scores, stream, ws);
   uint16_t* pb = nullptr;
-  hipError_t e = ws.get(2 * (size_t)n * kPatchPix, (void**)&pb);
+  e = ws.get(2 * (size_t)n * kPatchPix, (void**)&pb);
   if (e != hipSuccess) return hip_fail(e, "workspace (16-bit patches)");
   {
     KernelTimer kt("patches_to_16", stream);
