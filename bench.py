@@ -44,7 +44,7 @@ KERNELS = {
     "gather": ("bytes", "gather.hip"),
     "patches_to_16": ("bytes_cast", "gather.hip"),
     "conv_fp32": ("flops_conv", "fp32_vector.hip"),
-    "fc1_fp32": ("flops_fc1", "fp32_vector.hip"),
+    "fc1_fp32": ("flops_fc1", "fc1_f32.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
     "tail": ("bytes_tail", "tail.hip"),
 }
@@ -349,6 +349,8 @@ def main():
     model = KERNELS[dom][0]
     if model == "flops_conv_fc1":
         bound, peak = "mfma", PEAK["mfma_bf16"]       # fp16 and bf16 MFMA share one peak
+    elif model == "flops_fc1":
+        bound, peak = "mfma", PEAK["mfma_fp32"]
     elif model.startswith("flops"):
         bound, peak = "alu", PEAK["alu_fp32"]
     else:

@@ -225,7 +225,7 @@ class Workspace {
 // Scratch bytes of one call: 16-bit or fp32 patches (when the call makes
 // them), the FC1 split-K partials and, on the fp32 path, one chunk of maps.
 constexpr int kSplitsFp32 = 8;            // FC1 split-K on the vector fp32 path
-constexpr int64_t kChunkFp32 = 2048;      // patches whose maps are live at once
+constexpr int64_t kChunkFp32 = 4096;      // patches whose maps are live at once
 size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
   const bool half = precision != POINTID_FP32;
   size_t b = 0;
@@ -256,7 +256,7 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
     if (e != hipSuccess) return hip_fail(e, "conv launch");
     {
       KernelTimer kt("fc1_fp32", stream);
-      e = launch_fc1_fp32(act, m, c0, n, h->w, S, part, stream);
+      e = launch_fc1_f32(act, m, c0, n, h->w.fc1_wt, S, part, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "fc1 launch");
   }
@@ -425,7 +425,7 @@ int pointid_create(const pointid_weights* w, int precision, int device,
     pieces.push_back({nullptr, (size_t)kConvFrags * 16, (const void**)&hnd->w.conv_frag});
     pieces.push_back({nullptr, (size_t)kFc1Frags * 16, (const void**)&hnd->w.fc1_frag});
   } else {
-    pieces.push_back({w->fc1_w, sizeof(float) * kFc1In * kFc1Out, (const void**)&hnd->w.fc1_w});
+    pieces.push_back({nullptr, sizeof(float) * kFc1In * kFc1Out, (const void**)&hnd->w.fc1_wt});
   }
   size_t total = 0;
   std::vector<size_t> offs;
@@ -449,16 +449,19 @@ int pointid_create(const pointid_weights* w, int precision, int device,
       return hip_fail(e, "hipMemcpy(weights)");
     }
   }
-  if (half) {
-    // 16-bit fragments are packed on the device from a temporary fp32 FC1 copy
+  {
+    // FC1 is rearranged on the device from a temporary fp32 copy: 16-bit
+    // fragments for the MFMA kernel, or the transposed fp32 matrix
     float* w1 = nullptr;
     e = hipMalloc(&w1, sizeof(float) * kFc1In * kFc1Out);
     if (e == hipSuccess)
       e = hipMemcpy(w1, w->fc1_w, sizeof(float) * kFc1In * kFc1Out, hipMemcpyHostToDevice);
-    if (e == hipSuccess)
+    if (e == hipSuccess && half)
       e = launch_pack_16(precision == POINTID_FP16, hnd->w.conv_w, hnd->w.conv_b, w1,
                          const_cast<uint4*>(hnd->w.conv_frag), const_cast<uint4*>(hnd->w.fc1_frag),
                          nullptr);
+    if (e == hipSuccess && !half)
+      e = launch_transpose_w1(w1, const_cast<float*>(hnd->w.fc1_wt), nullptr);
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (w1) (void)hipFree(w1);
     if (e != hipSuccess) {

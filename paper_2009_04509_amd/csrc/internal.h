@@ -39,7 +39,7 @@ struct DeviceWeights {
   int precision;             // POINTID_FP32 / POINTID_BF16 / POINTID_FP16
   const float* conv_w;       // [48][25] fp32
   const float* conv_b;       // [48]
-  const float* fc1_w;        // [92928][128] fp32 (fp32 handles)
+  const float* fc1_wt;       // [128][92928] fp32, FC1 transposed (fp32 handles)
   const float* fc1_b;        // [128]
   const float* fc2_w;        // [128][32]
   const float* fc2_b;        // [32]
@@ -84,11 +84,14 @@ hipError_t launch_conv_fp32(const float* patches, int64_t n,
                             const DeviceWeights& w, float* act,
                             hipStream_t stream);
 
-// fp32 FC1 partial products: part[s][row0 + i][128] = sum over split s of
-// act[i][k] * fc1_w[k][n], for i < n.  `n_total` is the row count of `part`.
-hipError_t launch_fc1_fp32(const float* act, int64_t n, int64_t row0,
-                           int64_t n_total, const DeviceWeights& w, int splits,
-                           float* part, hipStream_t stream);
+// fp32 FC1 partial products on fp32 MFMA: part[s][row0 + i][128] = sum over
+// split s of act[i][k] * W1[k][o], for i < m, from the transposed weights
+// w1t[o][k].  `n_total` is the row count of `part`.
+hipError_t launch_fc1_f32(const float* act, int64_t m, int64_t row0, int64_t n_total,
+                          const float* w1t, int splits, float* part, hipStream_t stream);
+
+// w1t[o][k] = w1[k][o] for the FC1 weights.
+hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream);
 
 // Reduce the split-K partials in fixed order, then bias+ReLU, FC2+ReLU, the
 // softmax and sigmoid heads: scores [n][4].

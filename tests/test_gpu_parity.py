@@ -227,8 +227,6 @@ def test_classify_patches_config4(pid, handles, prec, batch):
 @pytest.mark.parametrize("batch", [16384, 65536])
 def test_classify_patches_large_sampled(pid, handles, prec, batch):
     h = _handle(handles, prec)
-    if prec == "fp32" and batch > 16384:
-        pytest.skip("vector-ALU fp32 path: 64k patches exceed the per-test time budget")
     P = synth.config4_patches(batch, seed=1004)
     say(f"classify_patches B={batch} {prec} sampled")
     got = pid.pointid_classify_patches(h, t(P)).cpu().numpy()
