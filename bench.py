@@ -43,8 +43,8 @@ PEAK = {"mfma_bf16": 2500.0, "mfma_fp32": 157.3, "alu_fp32": 157.3, "hbm": 8000.
 KERNELS = {
     "gather": ("bytes", "gather.hip"),
     "patches_to_16": ("bytes_cast", "gather.hip"),
-    "conv_fp32": ("flops_conv", "fp32_vector.hip"),
-    "fc1_fp32": ("flops_fc1", "fc1_f32.hip"),
+    "conv_fp32": ("flops_conv", "fp32_mfma.hip"),
+    "fc1_fp32": ("flops_fc1", "fp32_mfma.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
     "tail": ("bytes_tail", "tail.hip"),
 }
@@ -349,7 +349,7 @@ def main():
     model = KERNELS[dom][0]
     if model == "flops_conv_fc1":
         bound, peak = "mfma", PEAK["mfma_bf16"]       # fp16 and bf16 MFMA share one peak
-    elif model == "flops_fc1":
+    elif model in ("flops_fc1", "flops_conv"):
         bound, peak = "mfma", PEAK["mfma_fp32"]
     elif model.startswith("flops"):
         bound, peak = "alu", PEAK["alu_fp32"]

@@ -251,7 +251,7 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
     const int64_t m = (n - c0) < chunk ? (n - c0) : chunk;
     {
       KernelTimer kt("conv_fp32", stream);
-      e = launch_conv_fp32(patches + c0 * kPatchPix, m, h->w, act, stream);
+      e = launch_conv_f32(patches + c0 * kPatchPix, m, h->w, act, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "conv launch");
     {

@@ -1,4 +1,17 @@
-// FC1 of the fp32 path (paper §2.2) on fp32 MFMA: split-K partial products
+// The fp32 path's conv and FC1 (paper §2.2) on fp32 MFMA.
+//
+// Conv: maps act[p][(y*44 + x)*48 + k] = ReLU(b_k + sum_{u,v} K[k][u][v] P[y+u][x+v])
+// for a chunk of patches.  As in the 16-bit kernel, positions go in pairs
+// (x, x+1), x even, whose 5x6 window (30 pixels) plus a bias slot fills a K=32
+// operand, here 8 v_mfma_f32_16x16x4_f32 (slot f = 4i + g for MFMA i and lane
+// group g).  A = filter (16 channels x 4 slots; the fragment for position
+// x + s holds K[k][u][c - s] at slot f = 6u + c, and b_k at slot 30), B = window
+// (4 slots x 16 patches), C = 16 channels x 16 patches of one position: 6 conv
+// tiles (2 shifts x 3 channel tiles) per pair.  A block of 8 waves owns 16
+// patches; wave w takes the pairs w, w + 8, ...; the filter fragments stay in
+// registers and each lane writes its 4 channels of a tile as one 16-byte store.
+//
+// FC1: split-K partial products
 //   part[s][row0 + p][o] = sum over split s of act[p][k] * W1[k][o],
 // with the conv maps `act` [m][92928] (HWC flatten, written by the conv kernel)
 // and the weights stored transposed, W1t[o][k] = W1[k][o].
@@ -22,6 +35,76 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+// ---------------------------------------------------------------- conv
+constexpr int kConvWaves = 8;
+constexpr int kPairs = kPos / 2;              // 968
+constexpr int kPairsPerRow = kFm / 2;         // 22
+
+__global__ __launch_bounds__(kConvWaves * 64) void conv_f32_kernel(
+    const float* __restrict__ patches, int64_t m, const float* __restrict__ conv_w,
+    const float* __restrict__ conv_b, float* __restrict__ act) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, g = lane >> 4;
+  const int64_t p = (int64_t)blockIdx.x * 16 + col;
+  const float* src = patches + (p < m ? p : m - 1) * kPatchPix;   // past the end: the last patch, not stored
+  // filter fragments fa[s * 3 + t][i]: channel 16 t + col, slot f = 4 i + g
+  float fa[6][8];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int f = 4 * i + g, ch = 16 * t + col;
+        float v = 0.f;
+        if (f < 30) {
+          const int u = f / 6, c = f - (f / 6) * 6 - s;
+          if (c >= 0 && c < kK) v = conv_w[ch * kK * kK + u * kK + c];
+        } else if (f == 30) {
+          v = conv_b[ch];
+        }
+        fa[s * 3 + t][i] = v;
+      }
+  // window slot f of this lane: pixel offset (f < 30) or a constant
+  int woff[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int f = 4 * i + g;
+    woff[i] = f < 30 ? (f / 6) * kPatch + f - (f / 6) * 6 : 0;
+  }
+  float* dst = act + p * kFc1In + 4 * g;
+#pragma unroll 1
+  for (int P = wave; P < kPairs; P += kConvWaves) {
+    const int y = P / kPairsPerRow, x = 2 * (P - y * kPairsPerRow);
+    const float* w0 = src + y * kPatch + x;
+    float b[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int f = 4 * i + g;
+      b[i] = f < 30 ? w0[woff[i]] : (f == 30 ? 1.f : 0.f);
+    }
+    floatx4 c[6];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) c[k] = (floatx4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int k = 0; k < 6; ++k) c[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[k][i], b[i], c[k], 0, 0, 0);
+    if (p < m) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          const floatx4 v = c[s * 3 + t];
+          *reinterpret_cast<floatx4*>(dst + (y * kFm + x + s) * kCh + 16 * t) =
+              (floatx4){fmaxf(v[0], 0.f), fmaxf(v[1], 0.f), fmaxf(v[2], 0.f), fmaxf(v[3], 0.f)};
+        }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- FC1
 constexpr int kPB = 64;                      // patches per block
 constexpr int kKB = kFc1In / 16;             // 5808 blocks of 16 k
 constexpr int kDepth = 3;                    // load sets in flight
@@ -142,6 +225,15 @@ __global__ __launch_bounds__(256) void transpose_w1_kernel(const float* __restri
 }
 
 }  // namespace
+
+hipError_t launch_conv_f32(const float* patches, int64_t m, const DeviceWeights& w, float* act,
+                           hipStream_t stream) {
+  if (m <= 0) return hipSuccess;
+  const int64_t blocks = (m + 15) / 16;
+  conv_f32_kernel<<<dim3((unsigned)blocks), dim3(kConvWaves * 64), 0, stream>>>(patches, m, w.conv_w,
+                                                                                 w.conv_b, act);
+  return hipGetLastError();
+}
 
 hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream) {
   static_assert(kFc1In % 32 == 0 && kFc1Out % 32 == 0, "whole 32 x 32 tiles");

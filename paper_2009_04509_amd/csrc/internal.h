@@ -79,10 +79,9 @@ hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);
 
-// fp32 conv + ReLU for patches [n][2304] -> activations [n][92928] (HWC).
-hipError_t launch_conv_fp32(const float* patches, int64_t n,
-                            const DeviceWeights& w, float* act,
-                            hipStream_t stream);
+// fp32 conv + ReLU on fp32 MFMA for patches [m][2304] -> maps [m][92928] (HWC).
+hipError_t launch_conv_f32(const float* patches, int64_t m, const DeviceWeights& w, float* act,
+                           hipStream_t stream);
 
 // fp32 FC1 partial products on fp32 MFMA: part[s][row0 + i][128] = sum over
 // split s of act[i][k] * W1[k][o], for i < m, from the transposed weights
