@@ -281,6 +281,49 @@ def test_edge_hits_and_zero_bias(pid, handles, prec):
     hz.close()
 
 
+@pytest.mark.parametrize("prec", PRECS)
+def test_hits_path_matches_precut_patches_bitwise(pid, handles, prec):
+    """A hit's scores are those of its patch cut out beforehand (paper §2.1).
+
+    The 16-bit path builds patches inside the fused kernel from the image; the
+    pre-cut path reads fp32 patches.  Both must give the same bits for every
+    hit, whatever the image size, row pitch, base alignment or hit position
+    (inside, on the border, far outside, extreme int32 values, plane index
+    outside the table)."""
+    h = _handle(handles, prec)
+    for (W, T) in [(37, 101), (64, 100), (5, 7), (128, 512)]:
+        img = synth.coord_image(W, T) * np.float32(1e-3)
+        rng = np.random.default_rng(W + T)
+        hits = np.concatenate([
+            np.array([[0, 0], [W - 1, T - 1], [-30, 5], [W + 24, 3], [W + 23, 3], [3, -23],
+                      [3, -24], [3, T + 23], [W // 2, T // 2], [-24, -24],
+                      [-2**31, 2**31 - 1], [2**31 - 1, -2**31]]),
+            np.stack([rng.integers(-30, W + 30, 300), rng.integers(-30, T + 30, 300)], 1),
+        ]).astype(np.int32)
+        say(f"hits vs pre-cut {prec} W={W} T={T} ({len(hits)} hits)")
+        got = pid.pointid_classify(h, t(img), t(hits)).cpu().numpy()
+        ref = pid.pointid_classify_patches(h, t(oracle.gather_patches(img, hits))).cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    # image base 4 bytes past a 16-byte boundary
+    img = synth.coord_image(40, 64) * np.float32(1e-3)
+    buf = t(np.concatenate([[0.0], img.ravel()]).astype(np.float32))
+    view = buf[1:].view(40, 64)
+    hits = np.array([[0, 0], [20, 30], [39, 63], [10, 40]], np.int32)
+    got = pid.pointid_classify(h, view, t(hits)).cpu().numpy()
+    ref = pid.pointid_classify_patches(h, t(oracle.gather_patches(img, hits))).cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    # several planes, with plane indices outside the table
+    planes, h3 = cfg3()
+    sel = np.sort(np.random.default_rng(77).choice(len(h3), 2000, replace=False))
+    hh = h3[sel].copy()
+    hh[::97, 0] = len(planes)
+    hh[1::89, 0] = -1
+    got = pid.pointid_classify_planes(h, [t(p.image) for p in planes], t(hh)).cpu().numpy()
+    P = oracle.gather_patches_planes([p.image for p in planes], hh)
+    ref = pid.pointid_classify_patches(h, t(P)).cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
 def test_empty_calls(pid, handles):
     h = handles["fp32"]
     img = t(np.zeros((8, 8), np.float32))
