@@ -304,19 +304,22 @@ def main():
     pid.pointid_timing_reset()
     pid.pointid_timing_enable(True)
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # one event per step boundary: the first and last bracket the timed region,
+    # the others give the per-step distribution
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t_wall = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         step(h)
-    ev1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
     pid.pointid_timing_enable(False)
-    ms = ev0.elapsed_time(ev1)
+    ms = evs[0].elapsed_time(evs[-1])
     ms_step = ms / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})")
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f}; "
+        f"median {np.median(per_step):.3f}, min {per_step.min():.3f}, max {per_step.max():.3f})")
 
     patch_bytes = 9216 if args.precision == "fp32" else 4608
     kern = {}
@@ -367,6 +370,8 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "step_ms": {"median": round(float(np.median(per_step)), 4),
+                    "min": round(float(per_step.min()), 4), "max": round(float(per_step.max()), 4)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": args.precision, "data": "synthetic",
         "config": {**desc, "precision": args.precision},

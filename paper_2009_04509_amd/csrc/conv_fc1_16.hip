@@ -6,7 +6,8 @@
 // size in HBM traffic if written out and read back.  Here the conv is FC1's
 // operand producer: the maps exist only in registers.
 //
-// Work split.  A block owns 96 patches and one of kSplits contiguous ranges of
+// Work split.  A block owns 96 patches (32 in the blocks that finish a batch:
+// see conv_fc1_16_tiles) and one of kSplits contiguous ranges of
 // map positions (split-K); blockIdx % 8 selects the range, so every block on one
 // XCD reads the same 1/8 of the FC1 weights and that slice (2.97 MB) stays in
 // the XCD's 4 MB L2.  Positions are taken in pairs (x, x+1) with x even: the
@@ -48,34 +49,44 @@ constexpr int kNHalves = 2;                   // output halves
 constexpr int kWaves = kKGroups * kNHalves;   // 8
 constexpr int kThreads = kWaves * 64;         // 512
 constexpr int kMT = 8 / kNHalves;             // 16-output tiles per wave
-constexpr int kBt = 96;                       // patches per block
-constexpr int kTiles = kBt / 16;              // 16-patch MFMA tiles per block
-constexpr int kOwn = kTiles / kNHalves;       // tiles whose conv a wave computes
 constexpr int kPairsPerRow = kFm / 2;         // 22
 constexpr int kRing = 8;                      // patch-row ring slots
 // rows the first two steps of a split need: pairs P0 .. P0 + 2 kKGroups - 1 span
 // at most two map rows, plus the filter height
 constexpr int kPrologueRows = 2 + 5 - 1;
 constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
-constexpr int kSlot = kBt * kRP;              // dwords per ring slot
-// LDS layout (dwords): ring | conv filter fragments | swap buffers; the final
-// reduction reuses it from the start.
-constexpr int kConvOff = kRing * kSlot;                         // 19,968
-constexpr int kSwapOff = kConvOff + 6 * 64 * 4;                 // 21,504
-constexpr int kSwapWave = kOwn * 64 * 4;                        // one wave's fragments
-constexpr int kSwapBuf = kWaves * kSwapWave;                    // one buffer
-constexpr int kRegion = kMT * kTiles * 4 * 64;                  // one wave's partial sums
-constexpr int kMain = kSwapOff + 2 * kSwapBuf;                  // 33,792
-constexpr int kLdsDwords = (kMain > 4 * kRegion) ? kMain : 4 * kRegion;
+constexpr int kBigTile = 96;                  // patches per block (most blocks)
+constexpr int kSmallTile = 32;                // patches per block (the last ones)
 
-// One patch row (96 B) of each of the block's patches: kBt x 6 chunks of 16 B.
-// Chunk c = tid, plus c = kThreads + tid for the first kRowExtra threads (whole
-// waves, so no lane diverges).  Patches past the end of the batch are read from
-// the last patch instead: their results are never stored.
-constexpr int kRowChunks = kBt * 6;
-constexpr int kRowExtra = kRowChunks - kThreads;
-static_assert(kRowExtra > 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads, "row chunking");
+// Layout of a block of kBt patches.  LDS (dwords): ring | conv filter
+// fragments | swap buffers; the final reduction reuses it from the start.
+// A patch row (96 B) of each of the block's patches is kBt x 6 chunks of 16 B:
+// chunk c = tid for the first kRowMain threads, plus c = kThreads + tid for
+// the first kRowExtra threads (whole waves, so no lane diverges).
+template <int kBt>
+struct Tile {
+  static constexpr int kTiles = kBt / 16;                 // 16-patch MFMA tiles
+  static constexpr int kOwn = kTiles / kNHalves;          // tiles whose conv a wave computes
+  static constexpr int kSlot = kBt * kRP;                 // dwords per ring slot
+  static constexpr int kConvOff = kRing * kSlot;
+  static constexpr int kSwapOff = kConvOff + 6 * 64 * 4;
+  static constexpr int kSwapWave = kOwn * 64 * 4;         // one wave's fragments
+  static constexpr int kSwapBuf = kWaves * kSwapWave;     // one buffer
+  static constexpr int kRegion = kMT * kTiles * 4 * 64;   // one wave's partial sums
+  static constexpr int kMain = kSwapOff + 2 * kSwapBuf;
+  static constexpr int kLdsDwords = (kMain > 4 * kRegion) ? kMain : 4 * kRegion;
+  static constexpr int kRowChunks = kBt * 6;
+  static constexpr int kRowMain = kRowChunks < kThreads ? kRowChunks : kThreads;
+  static constexpr int kRowExtra = kRowChunks - kRowMain;
+  static_assert(kTiles % kNHalves == 0 && kOwn <= 3, "whole tiles per output half");
+  static_assert(kRowMain % 64 == 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads,
+                "row chunking in whole waves");
+};
+static_assert(Tile<kBigTile>::kLdsDwords >= Tile<kSmallTile>::kLdsDwords, "LDS sized by the big tile");
 
+// Patches past the end of the batch are read from the last patch instead:
+// their results are never stored.
+template <int kBt>
 __device__ __forceinline__ uint4 row_chunk_load(const uint16_t* __restrict__ patches, int64_t n,
                                                 int64_t p_base, int r, int c) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -88,40 +99,49 @@ __device__ __forceinline__ uint4 row_chunk_load(const uint16_t* __restrict__ pat
                                        patches + gp * kPatchPix + r * kPatch + h * 8)));
 }
 
+template <int kBt>
 __device__ __forceinline__ void row_chunk_store(uint32_t* lds, int r, int c, const uint4& v) {
   const int p = c / 6, h = c - (c / 6) * 6;
-  uint32_t* d = lds + (r & (kRing - 1)) * kSlot + p * kRP + h * 4;
+  uint32_t* d = lds + (r & (kRing - 1)) * Tile<kBt>::kSlot + p * kRP + h * 4;
   *reinterpret_cast<uint2*>(d) = make_uint2(v.x, v.y);
   *reinterpret_cast<uint2*>(d + 2) = make_uint2(v.z, v.w);
 }
 
+// `main` and `extra`: wave-uniform, whether this thread has a first / second chunk
+template <int kBt>
 __device__ __forceinline__ void row_load(const uint16_t* __restrict__ patches, int64_t n,
-                                         int64_t p_base, int r, bool extra, uint4 (&v)[2]) {
-  v[0] = row_chunk_load(patches, n, p_base, r, threadIdx.x);
-  if (extra) v[1] = row_chunk_load(patches, n, p_base, r, threadIdx.x + kThreads);
+                                         int64_t p_base, int r, bool main, bool extra,
+                                         uint4 (&v)[2]) {
+  if (main) v[0] = row_chunk_load<kBt>(patches, n, p_base, r, threadIdx.x);
+  if (extra) v[1] = row_chunk_load<kBt>(patches, n, p_base, r, threadIdx.x + kThreads);
 }
 
-__device__ __forceinline__ void row_store(uint32_t* lds, int r, bool extra, const uint4 (&v)[2]) {
-  row_chunk_store(lds, r, threadIdx.x, v[0]);
-  if (extra) row_chunk_store(lds, r, threadIdx.x + kThreads, v[1]);
+template <int kBt>
+__device__ __forceinline__ void row_store(uint32_t* lds, int r, bool main, bool extra,
+                                          const uint4 (&v)[2]) {
+  if (main) row_chunk_store<kBt>(lds, r, threadIdx.x, v[0]);
+  if (extra) row_chunk_store<kBt>(lds, r, threadIdx.x + kThreads, v[1]);
 }
 
-template <bool kFp16, int kSplits>
-__global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
+// One block: patches p_base .. p_base + kBt - 1 (clamped to the batch) and
+// position range `split`.
+template <bool kFp16, int kSplits, int kBt>
+__device__ __forceinline__ void conv_fc1_block(
+    uint32_t* lds, int split, int64_t p_base,
     const uint16_t* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
     const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
-  __shared__ __attribute__((aligned(16))) uint32_t lds[kLdsDwords];
+  using T = Tile<kBt>;
+  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot, kRegion = T::kRegion;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = wave % kKGroups;            // position group
   const int nh = wave / kKGroups;            // output half; also the half of the tiles it convolves
   const int partner = kg + kKGroups * (1 - nh);
-  const bool extra = wave < kRowExtra / 64;  // wave-uniform
+  const bool rmain = wave < T::kRowMain / 64;   // wave-uniform
+  const bool extra = wave < T::kRowExtra / 64;
   const int col = lane & 15;                 // MFMA column (patch within tile) / row
   const int grp = lane >> 4;                 // MFMA K-slot group
-  const int split = blockIdx.x % kSplits;
-  const int64_t p_base = (int64_t)(blockIdx.x / kSplits) * kBt;
   // split boundaries on whole steps of kKGroups pairs: every wave runs `steps` pairs
   constexpr int kGroups = kPos / 2 / kKGroups;          // 242
   const int G0 = (kGroups * split) / kSplits;
@@ -131,10 +151,10 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
 
   // conv filter fragments [shift][channel tile] in LDS; a K-step reads two
   // (copied below, with the first patch rows, so both loads are in flight together)
-  uint4* cwl = reinterpret_cast<uint4*>(lds + kConvOff);
+  uint4* cwl = reinterpret_cast<uint4*>(lds + T::kConvOff);
   static_assert(6 * 64 <= kThreads, "one filter chunk per thread");
   // swap buffers: [buffer][wave][own tile][lane] x 16 B
-  uint4* swp = reinterpret_cast<uint4*>(lds + kSwapOff);
+  uint4* swp = reinterpret_cast<uint4*>(lds + T::kSwapOff);
 
   // this lane's 4 window dwords: slot pair f = 8*grp + 2d -> pixel (u, c)
   int woff[4], wrow[4];
@@ -174,11 +194,11 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     if (tid < 6 * 64) fv = convp[tid];
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
-      if (r0 + j <= loaded_hi) row_load(patches, n, p_base, r0 + j, extra, v[j]);
+      if (r0 + j <= loaded_hi) row_load<kBt>(patches, n, p_base, r0 + j, rmain, extra, v[j]);
     if (tid < 6 * 64) cwl[tid] = fv;
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
-      if (r0 + j <= loaded_hi) row_store(lds, r0 + j, extra, v[j]);
+      if (r0 + j <= loaded_hi) row_store<kBt>(lds, r0 + j, rmain, extra, v[j]);
   }
   __syncthreads();
 
@@ -267,7 +287,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     uint4 rv[2];
     const int want_hi = top_row(step + 2);
     const bool new_row = want_hi > loaded_hi;
-    if (new_row) row_load(patches, n, p_base, want_hi, extra, rv);
+    if (new_row) row_load<kBt>(patches, n, p_base, want_hi, rmain, extra, rv);
 
     const int P = P0 + kKGroups * step + kg;
     uint4 win_next[kOwn];
@@ -319,16 +339,16 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
       nxt[0] = convert1(ca[0], cb[0]);
       __builtin_amdgcn_sched_barrier(0);
       oth_group(0);
-      nxt[1] = convert1(ca[1], cb[1]);
+      if constexpr (kOwn > 1) nxt[1] = convert1(ca[1], cb[1]);
       put1(buf ^ 1, 0, nxt[0]);
       __builtin_amdgcn_sched_barrier(0);
       oth_group(1);
-      nxt[2] = convert1(ca[2], cb[2]);
-      put1(buf ^ 1, 1, nxt[1]);
+      if constexpr (kOwn > 2) nxt[2] = convert1(ca[2], cb[2]);
+      if constexpr (kOwn > 1) put1(buf ^ 1, 1, nxt[1]);
       if (q == 1) fix_win(win_next);
       __builtin_amdgcn_sched_barrier(0);
       oth_group(2);
-      put1(buf ^ 1, 2, nxt[2]);
+      if constexpr (kOwn > 2) put1(buf ^ 1, 2, nxt[2]);
       __builtin_amdgcn_sched_barrier(0);
       oth_group(3);
       __builtin_amdgcn_sched_barrier(0);
@@ -341,7 +361,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
         // wave still reads; the barrier below publishes it before the step
         // that first needs it (two steps later).
         if (new_row) {
-          row_store(lds, want_hi, extra, rv);
+          row_store<kBt>(lds, want_hi, rmain, extra, rv);
           loaded_hi = want_hi;
         }
       }
@@ -404,24 +424,63 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
   }
 }
 
+// Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A
+// patch's sums do not depend on the size of the tile it is in: every MFMA
+// column and every reduction step is per patch.
+template <bool kFp16, int kSplits>
+__global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
+    const uint16_t* __restrict__ patches, int64_t n, int64_t n_big, const uint4* __restrict__ w1p,
+    const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Tile<kBigTile>::kLdsDwords];
+  const int split = blockIdx.x % kSplits;
+  const int64_t t = blockIdx.x / kSplits;
+  if (t < n_big)
+    conv_fc1_block<kFp16, kSplits, kBigTile>(lds, split, t * kBigTile, patches, n, w1p, convp,
+                                             part, row0, n_total);
+  else
+    conv_fc1_block<kFp16, kSplits, kSmallTile>(lds, split, n_big * kBigTile + (t - n_big) * kSmallTile,
+                                               patches, n, w1p, convp, part, row0, n_total);
+}
+
 constexpr int kSplits16 = 8;
 
 }  // namespace
 
 int conv_fc1_16_splits() { return kSplits16; }
 
+// One block per CU and (tile, split): the big tiles fill whole rounds of the
+// CUs; what is left (less than one round of big tiles) is cut into small tiles
+// when they fit in one round, which then ends in about half the time.
+void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
+  const int64_t per_round = cus >= kSplits16 ? cus / kSplits16 : 1;   // tiles per round
+  int64_t big = n / (kBigTile * per_round) * per_round;
+  const int64_t rest = n - big * kBigTile;
+  int64_t small = (rest + kSmallTile - 1) / kSmallTile;
+  if (small > per_round) {                   // more than one round of small tiles
+    big += (rest + kBigTile - 1) / kBigTile;
+    small = 0;
+  }
+  *n_big = big;
+  *n_small = small;
+}
+
 hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  const int64_t tiles = (n + kBt - 1) / kBt;
-  const dim3 grid((unsigned)(tiles * kSplits16));
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  int64_t n_big = 0, n_small = 0;
+  conv_fc1_16_tiles(n, cus, &n_big, &n_small);
+  const dim3 grid((unsigned)((n_big + n_small) * kSplits16));
   if (fp16)
     conv_fc1_16_kernel<true, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
-        patches, n, w1p, convp, part, row0, n_total);
+        patches, n, n_big, w1p, convp, part, row0, n_total);
   else
     conv_fc1_16_kernel<false, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
-        patches, n, w1p, convp, part, row0, n_total);
+        patches, n, n_big, w1p, convp, part, row0, n_total);
   return hipGetLastError();
 }
 

@@ -75,6 +75,9 @@ hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
 // Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
 // bits) -> part[s][row0 + i][128] for s < conv_fc1_16_splits().
 int conv_fc1_16_splits();
+// Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
+// then n_small of 32.
+void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
 hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);

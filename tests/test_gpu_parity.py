@@ -258,6 +258,22 @@ def test_permutation_determinism_duplicates(pid, handles, prec):
     assert np.array_equal(one[0].view(np.uint32), base[7].view(np.uint32))
 
 
+@pytest.mark.parametrize("prec", ["bf16", "fp16"])
+def test_tile_shapes_give_the_same_bits(pid, handles, prec):
+    """A patch's scores do not depend on the batch around it.
+
+    4,196 patches run as 32 tiles of 96 patches plus 4 tiles of 32 (the end of
+    the batch); the same patches classified in other batches land in other
+    tiles and tile shapes, and must give the same bits."""
+    h = _handle(handles, prec)
+    P = synth.config4_patches(4196, seed=2024)
+    say(f"tile shapes {prec}")
+    full = pid.pointid_classify_patches(h, t(P)).cpu().numpy().view(np.uint32)
+    for lo, hi in [(4096, 4196), (0, 96), (4000, 4196), (1, 2), (4195, 4196), (100, 3173)]:
+        part = pid.pointid_classify_patches(h, t(P[lo:hi])).cpu().numpy().view(np.uint32)
+        assert np.array_equal(part, full[lo:hi]), f"patches {lo}:{hi}"
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_edge_hits_and_zero_bias(pid, handles, prec):
     h = _handle(handles, prec)
