@@ -1,14 +1,17 @@
 // Patch construction (paper §2.1): for hit (w, t) the 48x48 patch
 // P[r][c] = image[w - 24 + r][t - 24 + c], zero outside the plane.
 //
-// One wavefront builds one patch in two phases through LDS:
-//   1. stage: the 48 rows of the window are read as 13 aligned 16-byte chunks
-//      per row (52 floats covering the 48 needed plus the 0-3 float misalignment
-//      of the window start), zero-filled wherever a pixel is outside the plane;
-//   2. emit: each lane reads 4 (fp32) or 8 (bf16) consecutive pixels of a patch
-//      row from LDS at the row's misalignment offset and writes one aligned
-//      16-byte store, so a wavefront writes 1 KiB of contiguous output per
-//      instruction.
+// One wavefront builds one patch; each lane writes whole 16-byte output chunks
+// (4 fp32 or 8 bf16/fp16 pixels of one patch row), so a wavefront writes 1 KiB
+// of contiguous output per store.  A chunk's pixels are read as the aligned
+// 16-byte words that cover them (the run starts 0-3 floats into the first
+// word) and shifted into place in registers: no LDS, no barrier, and all of a
+// lane's loads are in flight together.  The loads go through a buffer resource
+// that starts at the image's 16-byte-aligned base and ends with the image, so
+// a word outside it reads as 0; words partly outside a row hold pixels of the
+// neighbouring row (or bytes just outside the image, in the same 16-byte
+// block), and every pixel whose wire or tick is outside the plane is set to 0
+// after the load.  Planes of 2 GiB or more take a per-pixel path instead.
 // Values are copied, never computed (bf16 / fp16 output is the
 // round-to-nearest-even of the fp32 pixel), so the result is bit-exact.
 #include "pointid.h"
@@ -19,24 +22,24 @@ namespace pointid {
 namespace {
 
 constexpr int kWaves = 4;                 // patches per block (one per wave)
-constexpr int kChunks = 13;               // 16-byte chunks staged per row
-constexpr int kStageCols = kChunks * 4;   // 52 floats
-
-__device__ __forceinline__ int64_t mod4(int64_t x) { return ((x % 4) + 4) % 4; }
 
 template <int kOut>
 __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
                                                      const int32_t* __restrict__ hits,
                                                      int hit_stride, int64_t n,
                                                      void* __restrict__ out) {
-  __shared__ __attribute__((aligned(16))) float stage[kWaves][kPatch][kStageCols];
+  constexpr int kPix = (kOut == POINTID_FP32) ? 4 : 8;   // pixels per 16-byte chunk
+  constexpr int kPerRow = kPatch / kPix;                 // chunks per patch row
+  constexpr int kChunks = kPatch * kPerRow;              // chunks per patch
+  constexpr int kIter = (kChunks + 63) / 64;
+  constexpr int kWords = kPix / 4 + 1;                   // aligned words covering a chunk
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWaves + wave;
-  const bool active = i < n;
+  if (i >= n) return;                                    // wave-uniform
 
   int plane = 0, w = 0, t = 0;
-  if (active) {
+  {
     const int32_t* h = hits + i * hit_stride;
     if (hit_stride == 3) {
       plane = h[0];
@@ -47,72 +50,89 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
       t = h[1];
     }
   }
-  // one patch per wave: make the hit wave-uniform so plane lookups are scalar
+  // one patch per wave: the hit is wave-uniform, so plane lookups are scalar
   plane = __builtin_amdgcn_readfirstlane(plane);
   w = __builtin_amdgcn_readfirstlane(w);
   t = __builtin_amdgcn_readfirstlane(t);
-  const bool plane_ok = active && plane >= 0 && plane < planes.n;
-  const float* img = nullptr;
-  int W = 0, T = 1;
-  if (plane_ok) {
-    img = planes.p[plane].image;
-    W = planes.p[plane].n_wires;
-    T = planes.p[plane].n_ticks;
-  }
-  const bool base_aligned = (reinterpret_cast<uintptr_t>(img) & 15) == 0;
+  const bool plane_ok = plane >= 0 && plane < planes.n;
+  const float* img = plane_ok ? planes.p[plane].image : nullptr;
+  const int64_t W = plane_ok ? planes.p[plane].n_wires : 0;
+  const int64_t T = plane_ok ? planes.p[plane].n_ticks : 1;
+  const uint64_t base = reinterpret_cast<uint64_t>(img) & ~uint64_t(15);
+  const uint64_t lead = reinterpret_cast<uint64_t>(img) - base;       // 0, 4, 8 or 12
+  const uint64_t span = lead + 4 * (uint64_t)W * (uint64_t)T;         // bytes base .. image end
+  const bool small = span < (uint64_t(1) << 31);                      // wave-uniform
 
-  float(*st)[kStageCols] = stage[wave];
-  // ---- stage
-  for (int k = lane; k < kPatch * kChunks; k += 64) {
-    const int r = k / kChunks;
-    const int j = k - r * kChunks;
-    const int wire = w - kHalf + r;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (plane_ok && wire >= 0 && wire < W) {
-      const int64_t flat0 = (int64_t)wire * T + (t - kHalf);
-      const int64_t tick0 = (int64_t)(t - kHalf) - mod4(flat0) + 4 * j;
-      const float* rowp = img + (int64_t)wire * T;
-      if (base_aligned && tick0 >= 0 && tick0 + 3 < T) {
-        v = *reinterpret_cast<const float4*>(rowp + tick0);
-      } else {
-        float e[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int64_t tk = tick0 + q;
-          e[q] = (tk >= 0 && tk < T) ? rowp[tk] : 0.f;
-        }
-        v = make_float4(e[0], e[1], e[2], e[3]);
-      }
+  uint4* o = reinterpret_cast<uint4*>(static_cast<char*>(out) +
+                                      i * kPatchPix * (kOut == POINTID_FP32 ? 4 : 2));
+  auto emit = [&](int k, const float (&v)[kPix]) {
+    if (k >= kChunks) return;
+    if constexpr (kOut == POINTID_FP32) {
+      o[k] = make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                        __float_as_uint(v[3]));
+    } else {
+      using Op = Op16<kOut == POINTID_FP16>;
+      o[k] = make_uint4(Op::pack(v[0], v[1]), Op::pack(v[2], v[3]), Op::pack(v[4], v[5]),
+                        Op::pack(v[6], v[7]));
     }
-    *reinterpret_cast<float4*>(&st[r][4 * j]) = v;
-  }
-  __syncthreads();
-  if (!active) return;
-
-  // ---- emit
-  if constexpr (kOut == POINTID_FP32) {
-    float4* o = reinterpret_cast<float4*>(static_cast<float*>(out) + i * kPatchPix);
-    for (int k = lane; k < kPatch * 12; k += 64) {
-      const int r = k / 12;
-      const int c = (k - r * 12) * 4;
-      const int wire = w - kHalf + r;
-      const int off = (plane_ok && wire >= 0 && wire < W)
-                          ? (int)mod4((int64_t)wire * T + (t - kHalf)) : 0;
-      const float* s = &st[r][off + c];
-      o[k] = make_float4(s[0], s[1], s[2], s[3]);
+  };
+  if (small) {
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(base), (short)0, (int)span, 0x00020000);
+#pragma unroll
+    for (int it = 0; it < kIter; ++it) {
+      const int k = lane + 64 * it;
+      const int r = k / kPerRow, hc = k - (k / kPerRow) * kPerRow;
+      const int64_t wire = (int64_t)w - kHalf + r;
+      const int64_t tick0 = (int64_t)t - kHalf + kPix * hc;
+      const bool row_ok = k < kChunks && wire >= 0 && wire < W;
+      // byte offset of the chunk's first pixel from `base`; the words are read
+      // from the 16-byte boundary below it, `m` floats earlier
+      const int64_t rel = (int64_t)lead + 4 * (wire * T + tick0);
+      const int m = (int)((rel >> 2) & 3);
+      // offsets are taken mod 2^32: every offset at or past 2^31 is out of range
+      const uint32_t a0 = row_ok ? (uint32_t)(rel - 4 * m) : 0x80000000u;
+      floatx4 q[kWords];
+#pragma unroll
+      for (int j = 0; j < kWords; ++j)
+        q[j] = __builtin_bit_cast(floatx4,
+                                  __builtin_amdgcn_raw_buffer_load_b128(rsrc, a0 + 16u * j, 0, 0));
+      // pixel j of the chunk is word float m + j: two levels of dword selects
+      // (v_perm_b32 byte selects, which the compiler keeps as value operations)
+      const uint32_t sel1 = (m & 1) ? 0x07060504u : 0x03020100u;
+      const uint32_t sel2 = (m & 2) ? 0x07060504u : 0x03020100u;
+      uint32_t s1[kPix + 2];
+#pragma unroll
+      for (int j = 0; j < kPix + 2; ++j)
+        s1[j] = __builtin_amdgcn_perm(__float_as_uint(q[(j + 1) / 4][(j + 1) % 4]),
+                                      __float_as_uint(q[j / 4][j % 4]), sel1);
+      // columns j_lo <= j < j_hi of the chunk are inside the row
+      const int64_t lo64 = -tick0, hi64 = T - tick0;
+      const int j_lo = row_ok ? (int)(lo64 < 0 ? 0 : (lo64 > kPix ? kPix : lo64)) : kPix;
+      const int j_hi = (int)(hi64 < 0 ? 0 : (hi64 > kPix ? kPix : hi64));
+      float v[kPix];
+#pragma unroll
+      for (int j = 0; j < kPix; ++j) {
+        const uint32_t x = __builtin_amdgcn_perm(s1[j + 2], s1[j], sel2);
+        v[j] = (j >= j_lo && j < j_hi) ? __uint_as_float(x) : 0.f;
+      }
+      emit(k, v);
     }
   } else {
-    uint4* o = reinterpret_cast<uint4*>(static_cast<uint16_t*>(out) + i * kPatchPix);
-    for (int k = lane; k < kPatch * 6; k += 64) {
-      const int r = k / 6;
-      const int c = (k - r * 6) * 8;
-      const int wire = w - kHalf + r;
-      const int off = (plane_ok && wire >= 0 && wire < W)
-                          ? (int)mod4((int64_t)wire * T + (t - kHalf)) : 0;
-      const float* s = &st[r][off + c];
-      using Op = Op16<kOut == POINTID_FP16>;
-      o[k] = make_uint4(Op::pack(s[0], s[1]), Op::pack(s[2], s[3]), Op::pack(s[4], s[5]),
-                        Op::pack(s[6], s[7]));
+#pragma unroll 1
+    for (int it = 0; it < kIter; ++it) {
+      const int k = lane + 64 * it;
+      const int r = k / kPerRow, hc = k - (k / kPerRow) * kPerRow;
+      const int64_t wire = (int64_t)w - kHalf + r;
+      const int64_t tick0 = (int64_t)t - kHalf + kPix * hc;
+      const bool row_ok = k < kChunks && wire >= 0 && wire < W;
+      float v[kPix];
+#pragma unroll
+      for (int j = 0; j < kPix; ++j) {
+        const int64_t tk = tick0 + j;
+        v[j] = (row_ok && tk >= 0 && tk < T) ? img[wire * T + tk] : 0.f;
+      }
+      emit(k, v);
     }
   }
 }

@@ -165,6 +165,24 @@ def test_gather_unaligned_image_base(pid):
     assert np.array_equal(got, oracle.gather_patches(img, hits))
 
 
+def test_gather_plane_over_2gib(pid):
+    """A plane of more than 2 GiB takes the per-pixel path of the gather; its
+    patches must match the oracle bit for bit like any other plane's."""
+    W, T = 20000, 28000                                 # 2.24 GB of fp32
+    w = torch.arange(W, device=DEV, dtype=torch.int32).view(W, 1)
+    tt = torch.arange(T, device=DEV, dtype=torch.int32).view(1, T)
+    img = ((w * 7 + tt) % 4093).to(torch.float32)       # exact small integers
+    hits = np.array([[0, 0], [W - 1, T - 1], [W - 1, 0], [10000, 14000], [W + 3, 5],
+                     [19990, 27990], [5, T + 20], [12345, 1]], np.int32)
+    say(f"gather on a {W}x{T} plane ({4 * W * T / 2**30:.2f} GiB)")
+    got = pid.pointid_gather(img, t(hits), "fp32").cpu().numpy()
+    ref = oracle.gather_patches(img.cpu().numpy(), hits)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    gotb = pid.pointid_gather(img, t(hits), "bf16").cpu().numpy()
+    assert np.array_equal(gotb.view(np.uint16), _bits16(ref, "bf16"))
+    del img
+
+
 def test_gather_planes_config3(pid):
     planes, h3 = cfg3()
     say("gather config3 planes fp32+bf16")
