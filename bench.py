@@ -64,6 +64,11 @@ def parse():
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
     ap.add_argument("--streams", type=int, default=64, help="config 5: request streams")
     ap.add_argument("--per-stream", type=int, default=32, help="config 5: requests per stream")
+    ap.add_argument("--request-hits", type=int, nargs=2, default=[1000, 8000], metavar=("LO", "HI"),
+                    help="config 5: hits per request, uniform in [LO, HI]")
+    ap.add_argument("--batch-requests", type=int, default=0, metavar="K",
+                    help="config 5: merge the requests, in arrival order, into "
+                         "pointid_classify_requests calls of K requests (0: one call per request)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -193,15 +198,18 @@ def cpu_baseline(sample, n_sample):
 
 
 def serving(args, torch, pid, synth):
-    """Config 5: 8 resident config-2 planes; requests of 1,000-8,000 hits sent on
-    `--streams` streams, `--per-stream` each, enqueued round-robin.  One step
-    classifies every request; the value is hits per second of wall-clock time
-    from the first enqueue to the completion of the last request (host enqueue
-    cost included).  Per-request latency is the time between events recorded on
-    the request's stream just before and just after its call."""
+    """Config 5: 8 resident config-2 planes; requests of 1,000-8,000 hits (or
+    `--request-hits`) sent on `--streams` streams, `--per-stream` each, enqueued
+    round-robin.  One step classifies every request, one call per request, or
+    (`--batch-requests K`) K consecutive arrivals per batched call.  The value is
+    hits per second of wall-clock time from the first enqueue to the completion
+    of the last request (host enqueue cost included).  Per-request latency is
+    the time between events recorded on the stream just before and just after
+    the call that classified it."""
     dev = "cuda:0"
+    lo_hits, hi_hits = args.request_hits
     planes, reqs = synth.config5_requests(n_planes=8, n_streams=args.streams,
-                                          per_stream=args.per_stream)
+                                          per_stream=args.per_stream, lo=lo_hits, hi=hi_hits)
     imgs = [torch.from_numpy(p.image).to(dev) for p in planes]
     hits = [[torch.from_numpy(x).to(dev) for (_, x) in rs] for rs in reqs]
     outs = [[torch.empty((len(x), 4), dtype=torch.float32, device=dev) for (_, x) in rs]
@@ -210,17 +218,33 @@ def serving(args, torch, pid, synth):
     total = sum(len(x) for rs in reqs for (_, x) in rs)
     h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)
 
+    K = args.batch_requests
+    # arrival order: the k-th request of every stream, round-robin
+    order = [(s, k) for k in range(args.per_stream) for s in range(len(reqs))]
+
     def one_step():
         evs = []
-        for k in range(args.per_stream):
-            for s, rs in enumerate(reqs):
+        if K <= 0:
+            for s, k in order:
                 st = streams[s]
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(st)
-                pid.pointid_classify(h, imgs[rs[k][0]], hits[s][k], outs[s][k], stream=st)
+                pid.pointid_classify(h, imgs[reqs[s][k][0]], hits[s][k], outs[s][k], stream=st)
                 e1.record(st)
                 evs.append((e0, e1))
+            return evs
+        # batched: consecutive arrivals share one call; the calls rotate over
+        # the streams so that batches overlap as single requests do
+        for b in range(0, len(order), K):
+            st = streams[(b // K) % len(streams)]
+            batch = [(reqs[s][k][0], hits[s][k], outs[s][k]) for s, k in order[b:b + K]]
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            pid.pointid_classify_requests(h, imgs, batch, stream=st)
+            e1.record(st)
+            evs += [(e0, e1)] * len(batch)
         return evs
 
     log(f"[bench] serving: {args.streams} streams x {args.per_stream} requests, {total} hits; "
@@ -258,8 +282,11 @@ def serving(args, torch, pid, synth):
         "scaling": "weak", "vs_baseline": None, "dtype": args.precision, "data": "synthetic",
         "config": {"workload": f"serving: 8 resident planes (480 wires x 6000 ticks), "
                                f"{args.streams} streams x {args.per_stream} requests of "
-                               f"1,000-8,000 hits, one pointid_classify per request",
+                               f"{lo_hits:,}-{hi_hits:,} hits, " + (
+                                   f"batches of {K} requests per pointid_classify_requests call"
+                                   if K > 0 else "one pointid_classify per request"),
                    "hits": total, "requests": args.streams * args.per_stream,
+                   "batch_requests": K,
                    "precision": args.precision},
         "latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
                        "p99": round(float(np.percentile(lat, 99)), 4),

@@ -158,6 +158,35 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane *planes,
                             int32_t n_planes, const int32_t *hits,
                             int64_t n_hits, float *scores, void *stream);
 
+/* One request of a batched call. */
+typedef struct {
+    const int32_t *hits;   /* device int32: [n_hits][2] = (wire, tick) on plane
+                              `plane`, or [n_hits][3] = (plane, wire, tick)
+                              when plane < 0 */
+    int64_t n_hits;        /* >= 0; a request with no hits is skipped */
+    int32_t plane;         /* index into the call's planes, or -1 */
+    float *scores;         /* device fp32 [n_hits][4], 16-byte aligned */
+} pointid_request;
+
+/*
+ * Classify several independent requests in one launch sequence (paper §2.3:
+ * the server combines requests from many clients into larger batches, which
+ * §3.2 measures with dynamic batching).  The requests' hits are classified as
+ * one batch over the shared `planes`; each request's scores land in its own
+ * output, with exactly the bits pointid_classify (plane >= 0) or
+ * pointid_classify_planes (plane < 0) gives that request alone.  More than 64
+ * non-empty requests run as consecutive batches of 64.
+ *   planes    HOST array, 1 <= n_planes <= 64, read during the call only
+ *   requests  HOST array of n_requests, read during the call only
+ * Errors: EINVAL (NULL handle, planes or requests; n_requests < 0; a request
+ * with n_hits < 0, plane >= n_planes, or a NULL or misaligned pointer with
+ * n_hits > 0; a plane as in pointid_classify_planes), ENOMEM, EHIP.  Every
+ * request is checked before any is classified.
+ */
+int pointid_classify_requests(pointid_handle h, const pointid_plane *planes,
+                              int32_t n_planes, const pointid_request *requests,
+                              int32_t n_requests, void *stream);
+
 /*
  * Classify pre-cut patches (the model interface of paper §2.3, which receives
  * batches of ready patches).

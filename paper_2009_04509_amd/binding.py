@@ -52,6 +52,11 @@ class _Plane(ctypes.Structure):
                 ("n_ticks", ctypes.c_int32)]
 
 
+class _Request(ctypes.Structure):
+    _fields_ = [("hits", ctypes.c_void_p), ("n_hits", ctypes.c_int64),
+                ("plane", ctypes.c_int32), ("scores", ctypes.c_void_p)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
@@ -66,6 +71,8 @@ def _load():
         "pointid_classify": (cint, [vp, vp, i32, i32, vp, i64, vp, vp]),
         "pointid_classify_planes": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp, vp]),
         "pointid_classify_patches": (cint, [vp, vp, i64, vp, vp]),
+        "pointid_classify_requests": (cint, [vp, ctypes.POINTER(_Plane), i32,
+                                             ctypes.POINTER(_Request), i32, vp]),
         "pointid_gather": (cint, [vp, i32, i32, vp, i64, vp, cint, vp]),
         "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
         "pointid_timing_enable": (cint, [cint]),
@@ -84,7 +91,8 @@ def _load():
 
 lib = _load()
 EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_classify",
-            "pointid_classify_planes", "pointid_classify_patches", "pointid_gather",
+            "pointid_classify_planes", "pointid_classify_requests", "pointid_classify_patches",
+            "pointid_gather",
             "pointid_gather_planes", "pointid_timing_enable", "pointid_timing_reset",
             "pointid_timing_query", "pointid_last_error", "pointid_version")
 
@@ -238,6 +246,32 @@ def pointid_classify_planes(h: Handle, images, hits: torch.Tensor,
     _check(lib.pointid_classify_planes(h.raw, arr, len(images), _ptr(hits), n, _ptr(scores),
                                        _stream_ptr(stream, hits.device)))
     return scores
+
+
+def pointid_classify_requests(h: Handle, images, requests, stream=None):
+    """Classify several requests in one batched call.
+
+    ``requests`` is a list of ``(plane, hits, scores)``: ``plane`` an index into
+    ``images`` with int32 hits [n][2] = (wire, tick), or -1 with hits [n][3] =
+    (plane, wire, tick); ``scores`` a float32 [n][4] output, or None to allocate
+    one.  Returns the list of score tensors."""
+    arr = _plane_array(images)
+    reqs = (_Request * max(len(requests), 1))()
+    outs = []
+    dev = None
+    for i, (plane, hits, scores) in enumerate(requests):
+        plane = int(plane)
+        _need(hits, torch.int32, f"requests[{i}].hits", h.device, (2,) if plane >= 0 else (3,))
+        n = hits.shape[0]
+        if scores is None:
+            scores = torch.empty((n, 4), dtype=torch.float32, device=hits.device)
+        _need(scores, torch.float32, f"requests[{i}].scores", h.device, (4,))
+        reqs[i] = _Request(hits.data_ptr(), n, plane, scores.data_ptr())
+        outs.append(scores)
+        dev = hits.device
+    _check(lib.pointid_classify_requests(h.raw, arr, len(images), reqs, len(requests),
+                                         _stream_ptr(stream, dev)))
+    return outs
 
 
 def pointid_classify_patches(h: Handle, patches: torch.Tensor,

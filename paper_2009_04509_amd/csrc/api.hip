@@ -236,9 +236,10 @@ size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
   return b;
 }
 
-// fp32 handles: patches (fp32 [n][2304]) -> scores.
+// fp32 handles: patches (fp32 [n][2304]) -> scores, or into the outputs of the
+// requests of `reqs` when it is given.
 int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* scores,
-                     hipStream_t stream, Workspace& ws) {
+                     hipStream_t stream, Workspace& ws, const RequestTable* reqs = nullptr) {
   const int S = kSplitsFp32;
   float* part = nullptr;
   float* act = nullptr;
@@ -262,7 +263,8 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
   }
   {
     KernelTimer kt("tail", stream);
-    e = launch_tail(part, S, n, h->w, scores, stream);
+    e = reqs ? launch_tail_requests(part, S, h->w, *reqs, stream)
+             : launch_tail(part, S, n, h->w, scores, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "tail launch");
   return POINTID_OK;
@@ -270,7 +272,7 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
 
 // 16-bit handles: patches (bf16 or fp16 [n][2304]) -> scores.
 int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* scores,
-                   hipStream_t stream, Workspace& ws) {
+                   hipStream_t stream, Workspace& ws, const RequestTable* reqs = nullptr) {
   const int S = conv_fc1_16_splits();
   float* part = nullptr;
   hipError_t e = ws.get(sizeof(float) * (size_t)S * n * kFc1Out, (void**)&part);
@@ -283,7 +285,8 @@ int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* 
   if (e != hipSuccess) return hip_fail(e, "conv_fc1 launch");
   {
     KernelTimer kt("tail", stream);
-    e = launch_tail(part, S, n, h->w, scores, stream);
+    e = reqs ? launch_tail_requests(part, S, h->w, *reqs, stream)
+             : launch_tail(part, S, n, h->w, scores, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "tail launch");
   return POINTID_OK;
@@ -326,6 +329,30 @@ int check_planes(const pointid_plane* planes, int32_t n_planes, PlaneTable* t) {
     t->p[i].n_ticks = planes[i].n_ticks;
   }
   return POINTID_OK;
+}
+
+// One batch of at most kMaxRequests non-empty requests: their hits are
+// gathered into one patch buffer and classified together; the tail writes
+// every patch's scores into its request's output.
+int classify_request_batch(pointid_handle h, const PlaneTable& planes, const RequestTable& reqs,
+                           hipStream_t stream) {
+  const int64_t n = reqs.start[reqs.n];
+  if (n == 0) return POINTID_OK;
+  Workspace ws(h->scratch, stream);
+  hipError_t e = ws.reserve(scratch_bytes(h->precision, n, true));
+  if (e != hipSuccess) return hip_fail(e, "scratch buffer");
+  const bool half = h->precision != POINTID_FP32;
+  void* patches = nullptr;
+  e = ws.get((half ? 2 : 4) * (size_t)n * kPatchPix, &patches);
+  if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
+  {
+    KernelTimer kt("gather", stream);
+    e = launch_gather_requests(planes, reqs, patches, h->precision, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  if (half)
+    return run_network_16(h, static_cast<const uint16_t*>(patches), n, nullptr, stream, ws, &reqs);
+  return run_network_fp32(h, static_cast<const float*>(patches), n, nullptr, stream, ws, &reqs);
 }
 
 }  // namespace
@@ -531,6 +558,54 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane* planes, int32
   if (!hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
   if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
   return classify_hits(h, t, hits, 3, n_hits, scores, stream);
+}
+
+int pointid_classify_requests(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
+                              const pointid_request* requests, int32_t n_requests,
+                              void* stream_) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n_requests < 0) return fail(POINTID_EINVAL, "n_requests is negative");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (n_requests == 0) return POINTID_OK;
+  if (!requests) return fail(POINTID_EINVAL, "requests is NULL");
+  int64_t total = 0;
+  for (int32_t r = 0; r < n_requests; ++r) {
+    const pointid_request& q = requests[r];
+    const std::string at = "request " + std::to_string(r) + ": ";
+    if (q.n_hits < 0) return fail(POINTID_EINVAL, at + "n_hits is negative");
+    if (q.plane >= n_planes) return fail(POINTID_EINVAL, at + "plane index out of range");
+    if (q.n_hits == 0) continue;
+    if (!q.hits || !q.scores) return fail(POINTID_EINVAL, at + "NULL device pointer");
+    if (!aligned16(q.scores)) return fail(POINTID_EINVAL, at + "scores must be 16-byte aligned");
+    total += q.n_hits;
+  }
+  if (total == 0) return POINTID_OK;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  RequestTable tab;
+  std::memset(&tab, 0, sizeof(tab));
+  for (int32_t r = 0; r <= n_requests; ++r) {
+    // flush a full table, and the last one
+    if (r == n_requests || tab.n == kMaxRequests) {
+      if (tab.n > 0) {
+        rc = classify_request_batch(h, t, tab, stream);
+        if (rc != POINTID_OK) return rc;
+      }
+      std::memset(&tab, 0, sizeof(tab));
+      if (r == n_requests) break;
+    }
+    const pointid_request& q = requests[r];
+    if (q.n_hits == 0) continue;
+    tab.hits[tab.n] = q.hits;
+    tab.scores[tab.n] = q.scores;
+    tab.plane[tab.n] = q.plane < 0 ? -1 : q.plane;
+    tab.start[tab.n + 1] = tab.start[tab.n] + q.n_hits;
+    ++tab.n;
+  }
+  return POINTID_OK;
 }
 
 int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,

@@ -23,33 +23,65 @@ namespace {
 
 constexpr int kWaves = 4;                 // patches per block (one per wave)
 
-template <int kOut>
-__global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes,
-                                                     const int32_t* __restrict__ hits,
-                                                     int hit_stride, int64_t n,
+// Hit i of a hit array: (wire, tick) on plane 0 (stride 2) or (plane, wire, tick).
+struct HitArray {
+  const int32_t* hits;
+  int stride;
+  __device__ void get(int64_t i, int& plane, int& w, int& t) const {
+    const int32_t* h = hits + i * stride;
+    if (stride == 3) {
+      plane = h[0];
+      w = h[1];
+      t = h[2];
+    } else {
+      plane = 0;
+      w = h[0];
+      t = h[1];
+    }
+  }
+};
+
+// Hit i of a batch of requests: request r holds patches start[r] .. start[r+1]-1
+// (i is wave-uniform, so the search runs on scalar registers).
+struct RequestHits {
+  RequestTable tab;
+  __device__ void get(int64_t i, int& plane, int& w, int& t) const {
+    int lo = 0, hi = tab.n - 1;              // the last request starting at or before i
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (tab.start[mid] <= i) lo = mid;
+      else hi = mid - 1;
+    }
+    const int64_t j = i - tab.start[lo];
+    if (tab.plane[lo] >= 0) {
+      const int32_t* h = tab.hits[lo] + 2 * j;
+      plane = tab.plane[lo];
+      w = h[0];
+      t = h[1];
+    } else {
+      const int32_t* h = tab.hits[lo] + 3 * j;
+      plane = h[0];
+      w = h[1];
+      t = h[2];
+    }
+  }
+};
+
+template <int kOut, class Src>
+__global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src, int64_t n,
                                                      void* __restrict__ out) {
   constexpr int kPix = (kOut == POINTID_FP32) ? 4 : 8;   // pixels per 16-byte chunk
   constexpr int kPerRow = kPatch / kPix;                 // chunks per patch row
   constexpr int kChunks = kPatch * kPerRow;              // chunks per patch
   constexpr int kIter = (kChunks + 63) / 64;
   constexpr int kWords = kPix / 4 + 1;                   // aligned words covering a chunk
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kWaves + wave;
   if (i >= n) return;                                    // wave-uniform
 
   int plane = 0, w = 0, t = 0;
-  {
-    const int32_t* h = hits + i * hit_stride;
-    if (hit_stride == 3) {
-      plane = h[0];
-      w = h[1];
-      t = h[2];
-    } else {
-      w = h[0];
-      t = h[1];
-    }
-  }
+  src.get(i, plane, w, t);
   // one patch per wave: the hit is wave-uniform, so plane lookups are scalar
   plane = __builtin_amdgcn_readfirstlane(plane);
   w = __builtin_amdgcn_readfirstlane(w);
@@ -165,18 +197,30 @@ hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t*
   return hipGetLastError();
 }
 
-hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
-                         int hit_stride, int64_t n, void* out, int out_dtype,
-                         hipStream_t stream) {
+template <class Src>
+hipError_t launch_gather_src(const PlaneTable& planes, const Src& src, int64_t n, void* out,
+                             int out_dtype, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   const dim3 grid((unsigned)((n + kWaves - 1) / kWaves));
   if (out_dtype == POINTID_BF16)
-    gather_kernel<POINTID_BF16><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
+    gather_kernel<POINTID_BF16, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
   else if (out_dtype == POINTID_FP16)
-    gather_kernel<POINTID_FP16><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
+    gather_kernel<POINTID_FP16, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
   else
-    gather_kernel<POINTID_FP32><<<grid, dim3(256), 0, stream>>>(planes, hits, hit_stride, n, out);
+    gather_kernel<POINTID_FP32, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
   return hipGetLastError();
+}
+
+hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
+                         int hit_stride, int64_t n, void* out, int out_dtype,
+                         hipStream_t stream) {
+  return launch_gather_src(planes, HitArray{hits, hit_stride}, n, out, out_dtype, stream);
+}
+
+hipError_t launch_gather_requests(const PlaneTable& planes, const RequestTable& reqs, void* out,
+                                  int out_dtype, hipStream_t stream) {
+  if (reqs.n < 1 || reqs.n > kMaxRequests) return hipErrorInvalidValue;
+  return launch_gather_src(planes, RequestHits{reqs}, reqs.start[reqs.n], out, out_dtype, stream);
 }
 
 }  // namespace pointid

@@ -63,6 +63,23 @@ hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
                          int hit_stride, int64_t n, void* out, int out_dtype,
                          hipStream_t stream);
 
+// Several requests classified by one launch sequence (kernel argument, by
+// value): request r owns patches start[r] .. start[r + 1] - 1 of the launch;
+// its hits are (wire, tick) on plane[r] when plane[r] >= 0, else
+// (plane, wire, tick); its scores go to scores[r].
+constexpr int kMaxRequests = 64;
+struct RequestTable {
+  int64_t start[kMaxRequests + 1];
+  const int32_t* hits[kMaxRequests];
+  float* scores[kMaxRequests];
+  int32_t plane[kMaxRequests];
+  int32_t n;
+};
+
+// Gather of the hits of the requests of `reqs` into patches [start[n]][48][48].
+hipError_t launch_gather_requests(const PlaneTable& planes, const RequestTable& reqs, void* out,
+                                  int out_dtype, hipStream_t stream);
+
 // Round fp32 patches [n][2304] to bf16 or fp16 (RNE) bit patterns.
 hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t* out,
                                 hipStream_t stream);
@@ -100,5 +117,8 @@ hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream);
 hipError_t launch_tail(const float* part, int splits, int64_t n,
                        const DeviceWeights& w, float* scores,
                        hipStream_t stream);
+// The same, with patch p's scores written to its request's output.
+hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
+                                const RequestTable& reqs, hipStream_t stream);
 
 }  // namespace pointid

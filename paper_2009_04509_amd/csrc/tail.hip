@@ -35,13 +35,32 @@ __device__ __forceinline__ void add4(float4& a, const float4& v) {
   a.w += v.w;
 }
 
+// Where patch p's 4 scores go: a score array [n][4] ...
+struct PlainOut {
+  float* scores;
+  __device__ float* row(int64_t p) const { return scores + 4 * p; }
+};
+// ... or the output of the request holding it (a uniform scan of the table, so
+// every table read is scalar).
+struct RequestOut {
+  RequestTable tab;
+  __device__ float* row(int64_t p) const {
+    float* d = tab.scores[0] + 4 * (p - tab.start[0]);
+    for (int k = 1; k < tab.n; ++k)
+      if (p >= tab.start[k]) d = tab.scores[k] + 4 * (p - tab.start[k]);
+    return d;
+  }
+};
+
+template <class Out>
 __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
-                                                   int64_t n, DeviceWeights w,
-                                                   float* __restrict__ scores) {
+                                                   int64_t n, DeviceWeights w, Out out) {
   __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
   __shared__ __attribute__((aligned(16))) float W2s[kFc1Out * kFc2Out];
+  __shared__ float* dst[kRows];
   const int tid = threadIdx.x;
   const int64_t p0 = (int64_t)blockIdx.x * kRows;
+  if (tid < kRows && p0 + tid < n) dst[tid] = out.row(p0 + tid);
   // W2 (16 KiB) into LDS: 4 float4 per thread, coalesced
   for (int i = tid; i < kFc1Out * kFc2Out / 4; i += 256)
     reinterpret_cast<float4*>(W2s)[i] = reinterpret_cast<const float4*>(w.fc2_w)[i];
@@ -108,7 +127,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
       const float inv = 1.f / (e0 + e1 + e2);
       const float eq = expf(-fabsf(q));
       const float sig = (q >= 0.f) ? 1.f / (1.f + eq) : eq / (1.f + eq);
-      reinterpret_cast<float4*>(scores)[p0 + r] = make_float4(e0 * inv, e1 * inv, e2 * inv, sig);
+      *reinterpret_cast<float4*>(dst[r]) = make_float4(e0 * inv, e1 * inv, e2 * inv, sig);
     }
   }
 }
@@ -120,7 +139,18 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
   if (n <= 0) return hipSuccess;
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
-  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, scores);
+  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, PlainOut{scores});
+  return hipGetLastError();
+}
+
+hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
+                                const RequestTable& reqs, hipStream_t stream) {
+  if (reqs.n < 1 || reqs.n > kMaxRequests) return hipErrorInvalidValue;
+  const int64_t n = reqs.start[reqs.n];
+  if (n <= 0) return hipSuccess;
+  if (splits < 1) return hipErrorInvalidValue;
+  const int64_t blocks = (n + kRows - 1) / kRows;
+  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, RequestOut{reqs});
   return hipGetLastError();
 }
 

@@ -77,6 +77,36 @@ def test_planes_validation(b):
     assert L.pointid_gather_planes(good, 2, NULL, 0, NULL, 0, NULL) == b.POINTID_OK
 
 
+def test_requests_validation(b):
+    """Batched requests: every request is checked before the handle is used
+    (FAKE handles below are never dereferenced)."""
+    L = b.lib
+    P, R = b._Plane, b._Request
+    planes = (P * 2)(P(0x1000, 10, 10), P(0x2000, 4, 4))
+    ok = R(0x3000, 5, 0, 0x4000)
+    assert L.pointid_classify_requests(NULL, planes, 2, (R * 1)(ok), 1, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_requests(FAKE, planes, 2, (R * 1)(ok), -1, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_requests(FAKE, planes, 2, None, 1, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_requests(FAKE, planes, 0, (R * 1)(ok), 1, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_requests(FAKE, None, 2, (R * 1)(ok), 1, NULL) == b.POINTID_EINVAL
+    cases = [
+        (R(0x3000, -1, 0, 0x4000), "negative"),
+        (R(0x3000, 5, 2, 0x4000), "plane index"),
+        (R(0, 5, 0, 0x4000), "NULL"),
+        (R(0x3000, 5, -1, 0), "NULL"),
+        (R(0x3000, 5, 1, 0x4004), "aligned"),
+    ]
+    for bad, word in cases:
+        # a valid request first: nothing is classified before all are checked
+        arr = (R * 2)(ok, bad)
+        assert L.pointid_classify_requests(FAKE, planes, 2, arr, 2, NULL) == b.POINTID_EINVAL
+        assert word in b.pointid_last_error() and "request 1" in b.pointid_last_error()
+    # no requests, or only empty ones with NULL pointers, is a no-op
+    assert L.pointid_classify_requests(FAKE, planes, 2, None, 0, NULL) == b.POINTID_OK
+    empty = (R * 2)(R(0, 0, 0, 0), R(0, 0, -1, 0))
+    assert L.pointid_classify_requests(FAKE, planes, 2, empty, 2, NULL) == b.POINTID_OK
+
+
 def test_create_validation(b):
     L = b.lib
     out = ctypes.c_void_p(123)

@@ -1,0 +1,123 @@
+"""GPU: batched requests (pointid_classify_requests).
+
+Several requests classified in one batched call must each get exactly the bits
+the request gets when classified alone (pointid_classify for single-plane
+requests, pointid_classify_planes for multi-plane ones), whatever else is in the
+batch; sampled hits must match the fp64 oracle as in test_gpu_parity.
+"""
+
+import functools
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="module")
+def pid():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2009_04509_amd import binding
+    return binding
+
+
+@functools.lru_cache(maxsize=None)
+def weights():
+    return synth.he_normal_weights()
+
+
+@functools.lru_cache(maxsize=None)
+def planes():
+    return [synth.config2(2000 + p) for p in range(3)]
+
+
+def t(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def make_requests(rng, sizes):
+    """(plane, hits) per size: plane >= 0 with [n][2] hits on it, or -1 with
+    [n][3] hits over all planes (every 50th hit on a plane outside the table)."""
+    pl = planes()
+    out = []
+    for k, n in enumerate(sizes):
+        if k % 3 == 2:
+            p = rng.integers(0, len(pl), size=n)
+            h = np.stack([p] + [np.zeros(n, np.int64)] * 2, 1)
+            for i in range(n):
+                pool = pl[p[i]].hits
+                h[i, 1:] = pool[rng.integers(0, len(pool))]
+            h[::50, 0] = len(pl)
+            out.append((-1, h.astype(np.int32)))
+        else:
+            p = int(rng.integers(0, len(pl)))
+            pool = pl[p].hits
+            out.append((p, np.ascontiguousarray(pool[rng.integers(0, len(pool), size=n)])))
+    return out
+
+
+def alone(pid, h, imgs, plane, hits):
+    if plane >= 0:
+        return pid.pointid_classify(h, imgs[plane], t(hits)).cpu().numpy()
+    return pid.pointid_classify_planes(h, imgs, t(hits)).cpu().numpy()
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16", "fp16"])
+def test_batched_requests_bitwise(pid, prec):
+    h = pid.pointid_create(weights(), prec, 0)
+    imgs = [t(p.image) for p in planes()]
+    rng = np.random.default_rng(11)
+    sizes = [1, 17, 235, 0, 1693, 3000, 96, 97, 31, 2048]
+    reqs = make_requests(rng, sizes)
+    say(f"batched requests {prec}: {len(reqs)} requests, {sum(sizes)} hits")
+    outs = pid.pointid_classify_requests(h, imgs, [(p, t(x), None) for p, x in reqs])
+    for k, ((p, x), o) in enumerate(zip(reqs, outs)):
+        got = o.cpu().numpy()
+        if len(x) == 0:
+            assert got.shape == (0, 4)
+            continue
+        ref = alone(pid, h, imgs, p, x)
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), f"request {k}"
+    # sampled hits of the largest request (a multi-plane one) against the oracle
+    p, x = reqs[5]
+    assert p < 0
+    idx = np.sort(rng.choice(len(x), 256, replace=False))
+    P = oracle.gather_patches_planes([q.image for q in planes()], x[idx])
+    got = outs[5].cpu().numpy()[idx].astype(np.float64)
+    if prec == "bf16":
+        ref, tol = oracle.classify_16bit_emulated(P, weights(), "bf16"), 2e-3
+    else:
+        ref, tol = oracle.classify_patches(P, weights()), {"fp32": 1e-4, "fp16": 2e-2}[prec]
+    err = float(np.abs(got - np.asarray(ref, np.float64)).max())
+    say(f"[requests {prec}] 256 sampled hits: max|d|={err:.3g}")
+    assert err <= tol
+    h.close()
+
+
+def test_more_than_64_requests(pid):
+    """70 non-empty requests (and some empty ones) run as two batches."""
+    h = pid.pointid_create(weights(), "fp16", 0)
+    imgs = [t(p.image) for p in planes()]
+    rng = np.random.default_rng(12)
+    sizes = [int(s) for s in rng.integers(0, 300, size=75)]
+    sizes[3] = sizes[40] = 0
+    reqs = make_requests(rng, sizes)
+    say(f"{len(reqs)} requests, {sum(sizes)} hits")
+    outs = pid.pointid_classify_requests(h, imgs, [(p, t(x), None) for p, x in reqs])
+    for k, ((p, x), o) in enumerate(zip(reqs, outs)):
+        if len(x):
+            ref = alone(pid, h, imgs, p, x)
+            assert np.array_equal(o.cpu().numpy().view(np.uint32), ref.view(np.uint32)), f"request {k}"
+    h.close()
