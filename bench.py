@@ -69,6 +69,12 @@ def parse():
     ap.add_argument("--batch-requests", type=int, default=0, metavar="K",
                     help="config 5: merge the requests, in arrival order, into "
                          "pointid_classify_requests calls of K requests (0: one call per request)")
+    ap.add_argument("--clients", type=int, default=0, metavar="T",
+                    help="config 5: T host threads, each classifying its share of the requests "
+                         "one at a time and waiting for each (directly on its own stream, or "
+                         "through the dynamic batcher when --batch-requests K > 0)")
+    ap.add_argument("--batch-delay-us", type=int, default=200,
+                    help="config 5 with --clients: the batcher's longest wait for a fuller batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -205,7 +211,10 @@ def serving(args, torch, pid, synth):
     hits per second of wall-clock time from the first enqueue to the completion
     of the last request (host enqueue cost included).  Per-request latency is
     the time between events recorded on the stream just before and just after
-    the call that classified it."""
+    the call that classified it.  With `--clients T`, T host threads each
+    classify their share one request at a time and wait for it (the paper's
+    many client processes), directly or through the dynamic batcher; latency
+    is then the host time from the call (or submit) to the scores being ready."""
     dev = "cuda:0"
     lo_hits, hi_hits = args.request_hits
     planes, reqs = synth.config5_requests(n_planes=8, n_streams=args.streams,
@@ -222,7 +231,36 @@ def serving(args, torch, pid, synth):
     # arrival order: the k-th request of every stream, round-robin
     order = [(s, k) for k in range(args.per_stream) for s in range(len(reqs))]
 
+    T = args.clients
+    batcher = pid.Batcher(h, imgs, max_requests=K, max_delay_us=args.batch_delay_us) \
+        if (T > 0 and K > 0) else None
+
+    def client_step():
+        """T synchronous clients; per-request latency measured on the host."""
+        import threading
+        lat = [[] for _ in range(T)]
+
+        def client(c):
+            st = streams[c % len(streams)]
+            for s, k in order[c::T]:
+                t0 = time.perf_counter()
+                if batcher is not None:
+                    batcher.wait(batcher.submit(reqs[s][k][0], hits[s][k], outs[s][k]))
+                else:
+                    pid.pointid_classify(h, imgs[reqs[s][k][0]], hits[s][k], outs[s][k], stream=st)
+                    st.synchronize()
+                lat[c].append((time.perf_counter() - t0) * 1e3)
+
+        ths = [threading.Thread(target=client, args=(c,)) for c in range(T)]
+        for th in ths:
+            th.start()
+        for th in ths:
+            th.join()
+        return [x for l in lat for x in l]
+
     def one_step():
+        if T > 0:
+            return client_step()
         evs = []
         if K <= 0:
             for s, k in order:
@@ -261,7 +299,7 @@ def serving(args, torch, pid, synth):
         evs = one_step()
         torch.cuda.synchronize()
         walls.append(time.perf_counter() - t0)
-        lat += [a.elapsed_time(b) for a, b in evs]
+        lat += evs if T > 0 else [a.elapsed_time(b) for a, b in evs]
     pid.pointid_timing_enable(False)
     wall = float(np.sum(walls))
     value = total * args.steps / wall
@@ -283,16 +321,22 @@ def serving(args, torch, pid, synth):
         "config": {"workload": f"serving: 8 resident planes (480 wires x 6000 ticks), "
                                f"{args.streams} streams x {args.per_stream} requests of "
                                f"{lo_hits:,}-{hi_hits:,} hits, " + (
-                                   f"batches of {K} requests per pointid_classify_requests call"
+                                   f"{T} client threads, each waiting for its request; " if T > 0
+                                   else "") + (
+                                   (f"dynamic batcher (up to {K} requests, {args.batch_delay_us} us)"
+                                    if T > 0 else
+                                    f"batches of {K} requests per pointid_classify_requests call")
                                    if K > 0 else "one pointid_classify per request"),
                    "hits": total, "requests": args.streams * args.per_stream,
-                   "batch_requests": K,
+                   "batch_requests": K, "clients": T,
                    "precision": args.precision},
         "latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
                        "p99": round(float(np.percentile(lat, 99)), 4),
                        "mean": round(float(lat.mean()), 4)},
         "kernels": kern,
     }
+    if batcher is not None:
+        batcher.close()
     h.close()
     print(json.dumps(out), flush=True)
 

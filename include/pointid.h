@@ -188,6 +188,35 @@ int pointid_classify_requests(pointid_handle h, const pointid_plane *planes,
                               int32_t n_requests, void *stream);
 
 /*
+ * Dynamic batching (paper §2.3; measured in §3.2): requests submitted from
+ * any host threads are merged, in arrival order, into pointid_classify_requests
+ * calls of at most `max_requests` (1..4096) requests over the resident
+ * `planes`, issued on the batcher's own stream as soon as `max_requests` are
+ * pending or the oldest has waited `max_delay_us` microseconds.  Up to 4
+ * batches run at once.  A request's scores are those it gets alone, bit for
+ * bit.  The handle and the plane images must outlive the batcher; a request's
+ * hits and scores buffers must stay valid until its wait returns.
+ * create errors: EINVAL (NULL out, handle or planes; a bad plane; n_planes,
+ * max_requests or max_delay_us out of range), EHIP.
+ */
+typedef struct pointid_batcher_s *pointid_batcher;
+int pointid_batcher_create(pointid_handle h, const pointid_plane *planes,
+                           int32_t n_planes, int32_t max_requests,
+                           int32_t max_delay_us, pointid_batcher *out);
+/* Classify every pending request, wait for all, then free.  NULL is a no-op. */
+int pointid_batcher_destroy(pointid_batcher b);
+/* Queue one request (copied; its buffers are not).  *ticket identifies it.
+ * Errors: EINVAL (NULL argument, bad request as in pointid_classify_requests,
+ * batcher being destroyed). */
+int pointid_batcher_submit(pointid_batcher b, const pointid_request *req,
+                           uint64_t *ticket);
+/* Block until the request `ticket` is classified: its scores are then in
+ * device memory, visible to the host and to every stream.  Returns the status
+ * of its batch (EHIP or ENOMEM if that batch failed), or EINVAL for a ticket
+ * this batcher did not issue. */
+int pointid_batcher_wait(pointid_batcher b, uint64_t ticket);
+
+/*
  * Classify pre-cut patches (the model interface of paper §2.3, which receives
  * batches of ready patches).
  *   patches device fp32 [n][48][48] (row = wire, column = tick), 16-byte aligned

@@ -73,6 +73,12 @@ def _load():
         "pointid_classify_patches": (cint, [vp, vp, i64, vp, vp]),
         "pointid_classify_requests": (cint, [vp, ctypes.POINTER(_Plane), i32,
                                              ctypes.POINTER(_Request), i32, vp]),
+        "pointid_batcher_create": (cint, [vp, ctypes.POINTER(_Plane), i32, i32, i32,
+                                          ctypes.POINTER(vp)]),
+        "pointid_batcher_destroy": (cint, [vp]),
+        "pointid_batcher_submit": (cint, [vp, ctypes.POINTER(_Request),
+                                          ctypes.POINTER(ctypes.c_uint64)]),
+        "pointid_batcher_wait": (cint, [vp, ctypes.c_uint64]),
         "pointid_gather": (cint, [vp, i32, i32, vp, i64, vp, cint, vp]),
         "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
         "pointid_timing_enable": (cint, [cint]),
@@ -92,6 +98,8 @@ def _load():
 lib = _load()
 EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_classify",
             "pointid_classify_planes", "pointid_classify_requests", "pointid_classify_patches",
+            "pointid_batcher_create", "pointid_batcher_destroy", "pointid_batcher_submit",
+            "pointid_batcher_wait",
             "pointid_gather",
             "pointid_gather_planes", "pointid_timing_enable", "pointid_timing_reset",
             "pointid_timing_query", "pointid_last_error", "pointid_version")
@@ -272,6 +280,56 @@ def pointid_classify_requests(h: Handle, images, requests, stream=None):
     _check(lib.pointid_classify_requests(h.raw, arr, len(images), reqs, len(requests),
                                          _stream_ptr(stream, dev)))
     return outs
+
+
+class Batcher:
+    """Dynamic batcher over a handle and resident plane images (see
+    pointid_batcher_create).  submit() returns a ticket; wait(ticket) blocks
+    until that request's scores are written.  The hits and scores tensors of a
+    request are kept alive here until its wait returns."""
+
+    def __init__(self, h: Handle, images, max_requests: int = 64, max_delay_us: int = 200):
+        self._arr = _plane_array(images)
+        self._images = list(images)
+        self._h = h
+        raw = ctypes.c_void_p()
+        _check(lib.pointid_batcher_create(h.raw, self._arr, len(images), int(max_requests),
+                                          int(max_delay_us), ctypes.byref(raw)))
+        self.raw = raw
+        self._live = {}
+
+    def submit(self, plane: int, hits: torch.Tensor, scores: torch.Tensor | None = None) -> int:
+        plane = int(plane)
+        _need(hits, torch.int32, "hits", self._h.device, (2,) if plane >= 0 else (3,))
+        n = hits.shape[0]
+        if scores is None:
+            scores = torch.empty((n, 4), dtype=torch.float32, device=hits.device)
+        _need(scores, torch.float32, "scores", self._h.device, (4,))
+        req = _Request(hits.data_ptr(), n, plane, scores.data_ptr())
+        ticket = ctypes.c_uint64()
+        _check(lib.pointid_batcher_submit(self.raw, ctypes.byref(req), ctypes.byref(ticket)))
+        self._live[ticket.value] = (hits, scores)
+        return ticket.value
+
+    def wait(self, ticket: int) -> torch.Tensor:
+        """Blocks until the request is classified; returns its scores tensor."""
+        try:
+            _check(lib.pointid_batcher_wait(self.raw, ctypes.c_uint64(ticket)))
+        finally:
+            pair = self._live.pop(ticket, None)
+        return pair[1] if pair else None
+
+    def close(self):
+        if self.raw:
+            _check(lib.pointid_batcher_destroy(self.raw))
+            self.raw = None
+            self._live.clear()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def pointid_classify_patches(h: Handle, patches: torch.Tensor,

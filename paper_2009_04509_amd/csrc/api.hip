@@ -357,6 +357,11 @@ int classify_request_batch(pointid_handle h, const PlaneTable& planes, const Req
 
 }  // namespace
 
+namespace pointid {
+int set_error(int code, const std::string& msg) { return fail(code, msg); }
+int handle_device(pointid_handle h) { return h->device; }
+}  // namespace pointid
+
 extern "C" {
 
 const char* pointid_last_error(void) { return g_err.c_str(); }

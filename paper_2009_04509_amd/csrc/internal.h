@@ -2,7 +2,11 @@
 // Not installed; nothing here is part of the public ABI.
 #pragma once
 
+#include <string>
+
 #include <hip/hip_runtime.h>
+
+#include "pointid.h"
 
 #include <cstdint>
 
@@ -91,6 +95,11 @@ hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
 
 // Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
 // bits) -> part[s][row0 + i][128] for s < conv_fc1_16_splits().
+// Error text for pointid_last_error (this thread); returns `code`.
+int set_error(int code, const std::string& msg);
+// Device ordinal of a handle.
+int handle_device(pointid_handle h);
+
 int conv_fc1_16_splits();
 // Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
 // then n_small of 32.

@@ -107,6 +107,29 @@ def test_requests_validation(b):
     assert L.pointid_classify_requests(FAKE, planes, 2, empty, 2, NULL) == b.POINTID_OK
 
 
+def test_batcher_validation(b):
+    """Batcher entry points reject bad arguments before using the handle."""
+    L = b.lib
+    P, R = b._Plane, b._Request
+    planes = (P * 1)(P(0x1000, 10, 10))
+    out = ctypes.c_void_p(0x1234)
+    assert L.pointid_batcher_create(NULL, planes, 1, 64, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert out.value is None                     # cleared on failure
+    assert L.pointid_batcher_create(FAKE, planes, 1, 64, 100, None) == b.POINTID_EINVAL
+    assert L.pointid_batcher_create(FAKE, None, 1, 64, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_create(FAKE, planes, 0, 64, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_create(FAKE, planes, 1, 0, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_create(FAKE, planes, 1, 5000, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_create(FAKE, planes, 1, 64, -1, ctypes.byref(out)) == b.POINTID_EINVAL
+    bad = (P * 1)(P(0, 10, 10))
+    assert L.pointid_batcher_create(FAKE, bad, 1, 64, 100, ctypes.byref(out)) == b.POINTID_EINVAL
+    t = ctypes.c_uint64()
+    req = R(0x3000, 5, 0, 0x4000)
+    assert L.pointid_batcher_submit(NULL, ctypes.byref(req), ctypes.byref(t)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_wait(NULL, 1) == b.POINTID_EINVAL
+    assert L.pointid_batcher_destroy(NULL) == b.POINTID_OK
+
+
 def test_create_validation(b):
     L = b.lib
     out = ctypes.c_void_p(123)

@@ -121,3 +121,75 @@ def test_more_than_64_requests(pid):
             ref = alone(pid, h, imgs, p, x)
             assert np.array_equal(o.cpu().numpy().view(np.uint32), ref.view(np.uint32)), f"request {k}"
     h.close()
+
+
+@pytest.mark.parametrize("prec", ["bf16", "fp16"])
+def test_batcher_threads_bitwise(pid, prec):
+    """Requests submitted from 4 host threads through the dynamic batcher get
+    the bits they get alone."""
+    import threading
+    h = pid.pointid_create(weights(), prec, 0)
+    imgs = [t(p.image) for p in planes()]
+    torch.cuda.synchronize()
+    per_thread = []
+    for k in range(4):
+        rng = np.random.default_rng(100 + k)
+        sizes = [int(s) for s in rng.integers(0, 2500, size=25)]
+        sizes[0] = 0
+        per_thread.append(make_requests(rng, sizes))
+    b = pid.Batcher(h, imgs, max_requests=16, max_delay_us=300)
+    results = [[None] * len(r) for r in per_thread]
+    errors = []
+
+    def client(k):
+        try:
+            # a few requests in flight per client, then wait for them in order
+            tickets = []
+            for i, (p, x) in enumerate(per_thread[k]):
+                tickets.append((i, b.submit(p, t(x))))
+                if len(tickets) == 3:
+                    i0, tk = tickets.pop(0)
+                    results[k][i0] = b.wait(tk).cpu().numpy()
+            for i0, tk in tickets:
+                results[k][i0] = b.wait(tk).cpu().numpy()
+        except Exception as e:      # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=client, args=(k,)) for k in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    b.close()
+    assert not errors, errors
+    n = 0
+    for k in range(4):
+        for i, (p, x) in enumerate(per_thread[k]):
+            got = results[k][i]
+            if len(x) == 0:
+                assert got.shape == (0, 4)
+                continue
+            ref = alone(pid, h, imgs, p, x)
+            assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), f"client {k} request {i}"
+            n += 1
+    say(f"batcher {prec}: {n} requests from 4 threads, all equal to single calls")
+    h.close()
+
+
+def test_batcher_destroy_drains(pid):
+    """Requests still pending when the batcher is destroyed are classified."""
+    h = pid.pointid_create(weights(), "fp16", 0)
+    imgs = [t(p.image) for p in planes()]
+    rng = np.random.default_rng(13)
+    reqs = make_requests(rng, [300, 7, 1200, 64, 5])
+    b = pid.Batcher(h, imgs, max_requests=64, max_delay_us=1000000)   # never due by time
+    outs = []
+    for p, x in reqs:
+        sc = torch.full((len(x), 4), float("nan"), device=DEV)
+        b.submit(p, t(x), sc)
+        outs.append(sc)
+    b.close()                        # launches the partial batch and waits for it
+    for (p, x), sc in zip(reqs, outs):
+        ref = alone(pid, h, imgs, p, x)
+        assert np.array_equal(sc.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    h.close()
