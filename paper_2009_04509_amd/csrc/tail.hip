@@ -21,6 +21,8 @@ namespace {
 constexpr int kRows = 32;                   // patches per block
 constexpr int kMaxSplits = 8;               // splits whose loads are in flight together
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
+typedef float vec4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) vec4 global_float4;
 
 __device__ __forceinline__ float sum32(float v) {
 #pragma unroll
@@ -57,10 +59,12 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
                                                    int64_t n, DeviceWeights w, Out out) {
   __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
   __shared__ __attribute__((aligned(16))) float W2s[kFc1Out * kFc2Out];
-  __shared__ float* dst[kRows];
+  // output rows, kept as global-address-space pointers so that the stores
+  // are global (not flat) stores
+  __shared__ global_float4* dst[kRows];
   const int tid = threadIdx.x;
   const int64_t p0 = (int64_t)blockIdx.x * kRows;
-  if (tid < kRows && p0 + tid < n) dst[tid] = out.row(p0 + tid);
+  if (tid < kRows && p0 + tid < n) dst[tid] = reinterpret_cast<global_float4*>(reinterpret_cast<uintptr_t>(out.row(p0 + tid)));
   // W2 (16 KiB) into LDS: 4 float4 per thread, coalesced
   for (int i = tid; i < kFc1Out * kFc2Out / 4; i += 256)
     reinterpret_cast<float4*>(W2s)[i] = reinterpret_cast<const float4*>(w.fc2_w)[i];
@@ -127,7 +131,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
       const float inv = 1.f / (e0 + e1 + e2);
       const float eq = expf(-fabsf(q));
       const float sig = (q >= 0.f) ? 1.f / (1.f + eq) : eq / (1.f + eq);
-      *reinterpret_cast<float4*>(dst[r]) = make_float4(e0 * inv, e1 * inv, e2 * inv, sig);
+      *dst[r] = (vec4){e0 * inv, e1 * inv, e2 * inv, sig};
     }
   }
 }
