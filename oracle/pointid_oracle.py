@@ -20,6 +20,14 @@ What it computes, with the passage each step follows:
   has a bias (the paper's parameter count of 11,900,420 requires all six), and
   the 44x44x48 maps are flattened channels-last, index (y*44 + x)*48 + k.
 
+* Hit finding, paper §2.1: the reconstruction finds wire hits on the
+  deconvolved waveforms (giving peak time and charge) before they are
+  classified; the paper names no algorithm.  Reading used here: a hit is a tick
+  whose value exceeds a threshold and is a local maximum along its wire's
+  waveform — greater than the tick before it and not less than the tick after
+  it, with ticks outside the waveform counting as minus infinity (a plateau
+  gives one hit, at its first tick).  Comparisons are exact in float32.
+
 All arithmetic is float64 with no intermediate rounding; each output is rounded
 to float32 once at the end.  Matrix products use numpy's ``@`` (a library
 primitive) with no blocking or reordering of our own.  Large inputs are
@@ -84,6 +92,32 @@ def gather_patches_planes(images, hits3) -> np.ndarray:
         if sel.size:
             out[sel] = gather_patches(img, hits3[sel, 1:3])
     return out
+
+
+# --------------------------------------------------------------------------
+# Hit finding (paper §2.1; the reading is in the module docstring)
+# --------------------------------------------------------------------------
+
+def find_hits(images, threshold) -> np.ndarray:
+    """int32 [n][3] = (plane, wire, tick) of every hit of every plane image
+    ([n_wires][n_ticks] float32), in plane, then wire, then tick order.
+
+    A tick t of wire w is a hit when x[t] > threshold, x[t] > x[t-1] and
+    x[t] >= x[t+1], where x[-1] and x[n_ticks] are minus infinity.
+    """
+    thr = np.float32(threshold)
+    out = []
+    for p, img in enumerate(images):
+        x = np.asarray(img, dtype=np.float32)
+        before = np.full_like(x, -np.inf)
+        before[:, 1:] = x[:, :-1]
+        after = np.full_like(x, -np.inf)
+        after[:, :-1] = x[:, 1:]
+        w, t = np.nonzero((x > thr) & (x > before) & (x >= after))    # row-major order
+        out.append(np.stack([np.full_like(w, p), w, t], axis=1))
+    if not out:
+        return np.zeros((0, 3), np.int32)
+    return np.concatenate(out, axis=0).astype(np.int32)
 
 
 def to_bf16_rne(x) -> np.ndarray:

@@ -339,3 +339,56 @@ def test_16bit_emulation_rounds_the_right_operands():
         full = oracle.forward(P, w)
         d = np.abs(full - oracle.forward_16bit_emulated(P, w, kind)).max()
         assert 0 < d < 2e-2
+
+
+# ------------------------------------------------------------------ hit finding
+
+def _hits_bruteforce(images, thr):
+    """Pure-Python loops over every tick, straight from the definition."""
+    out = []
+    thr = float(np.float32(thr))
+    for p, img in enumerate(images):
+        W, T = img.shape
+        for w in range(W):
+            for t in range(T):
+                x = float(img[w, t])
+                before = float(img[w, t - 1]) if t > 0 else -np.inf
+                after = float(img[w, t + 1]) if t + 1 < T else -np.inf
+                if x > thr and x > before and x >= after:
+                    out.append((p, w, t))
+    return np.array(out, np.int32).reshape(-1, 3)
+
+
+def test_hit_finding_worked_cases():
+    cases = json.load(open(os.path.join(GOLDEN, "hit_finding.json")))["cases"]
+    for c in cases:
+        img = np.array([c["wave"]], np.float32)
+        got = oracle.find_hits([img], c["threshold"])
+        assert got[:, 2].tolist() == c["ticks"], c
+        assert (got[:, :2] == 0).all()
+
+
+def test_hit_finding_matches_bruteforce_with_ties():
+    rng = np.random.default_rng(7)
+    # small integers, so that equal neighbours (plateaus) and values equal to
+    # the threshold are frequent
+    imgs = [rng.integers(-3, 6, size=(5, 40)).astype(np.float32),
+            rng.integers(0, 3, size=(3, 17)).astype(np.float32),
+            rng.normal(0, 2.5, size=(4, 64)).astype(np.float32)]
+    for thr in (-1.0, 0.0, 2.0, 3.5):
+        got = oracle.find_hits(imgs, thr)
+        ref = _hits_bruteforce(imgs, thr)
+        assert np.array_equal(got, ref), thr
+
+
+def test_hit_finding_single_pulse_and_order():
+    # one Gaussian pulse per wire on a quiet waveform: exactly one hit, at the
+    # peak; hits come out in plane, wire, tick order
+    T = 200
+    t = np.arange(T)
+    a = np.stack([50 * np.exp(-0.5 * ((t - c) / 3.0) ** 2) for c in (20, 150, 77)]).astype(np.float32)
+    b = np.zeros((2, T), np.float32)
+    b[1, [5, 190]] = 9.0
+    got = oracle.find_hits([a, b], 1.0)
+    assert got.tolist() == [[0, 0, 20], [0, 1, 150], [0, 2, 77], [1, 1, 5], [1, 1, 190]]
+    assert oracle.find_hits([b], 9.0).shape == (0, 3)       # equal to the threshold
