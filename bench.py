@@ -47,6 +47,9 @@ KERNELS = {
     "fc1_fp32": ("flops_fc1", "fp32_mfma.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
     "tail": ("bytes_tail", "tail.hip"),
+    "hits_mask": ("bytes_hits_mask", "hits.hip"),
+    "hits_scan": ("bytes_hits_scan", "hits.hip"),
+    "hits_emit": ("bytes_hits_emit", "hits.hip"),
 }
 
 
@@ -75,6 +78,9 @@ def parse():
                          "through the dynamic batcher when --batch-requests K > 0)")
     ap.add_argument("--batch-delay-us", type=int, default=200,
                     help="config 5 with --clients: the batcher's longest wait for a fuller batch")
+    ap.add_argument("--find-hits", type=float, default=None, metavar="THR",
+                    help="config 3: time hit finding (pointid_find_hits) on the event's 18 "
+                         "planes at threshold THR instead of classification")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -341,6 +347,98 @@ def serving(args, torch, pid, synth):
     print(json.dumps(out), flush=True)
 
 
+def hit_finding(args, torch, pid, synth):
+    """Config 3 planes: one step finds every hit of the event's 18 planes
+    (pointid_find_hits, three launches).  Algorithmic bytes of a step: the image
+    read once, plus 12 B written per hit found."""
+    import oracle
+    dev = "cuda:0"
+    thr = float(args.find_hits)
+    planes, _ = synth.config3()
+    imgs_np = [p.image for p in planes]
+    imgs = [torch.from_numpy(a).to(dev) for a in imgs_np]
+    image_bytes = sum(a.nbytes for a in imgs_np)
+    rows = sum(a.shape[0] for a in imgs_np)
+    h = pid.pointid_create(synth.he_normal_weights(), "fp16", 0)
+    cap = 8 << 20
+    out = torch.empty((cap, 3), dtype=torch.int32, device=dev)
+    n_found = torch.empty((1,), dtype=torch.int64, device=dev)
+
+    def step():
+        pid.pointid_find_hits(h, imgs, thr, capacity=cap, hits_out=out, n_found=n_found)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n_hits = int(n_found.item())
+    pid.pointid_timing_reset()
+    pid.pointid_timing_enable(True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record()
+    for i in range(args.steps):
+        step()
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    pid.pointid_timing_enable(False)
+    ms_step = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    mask_bytes = rows * 24 * 32
+    work = {"hits_mask": image_bytes + mask_bytes + 4 * rows,
+            "hits_scan": 4 * rows + 8 * rows + 8,
+            "hits_emit": mask_bytes + 4 * rows + 8 * rows + 12 * n_hits}
+    kern = {}
+    for name, wb in work.items():
+        tot, cnt = pid.pointid_timing_query(name)
+        if cnt:
+            kern[name] = {"ms_per_step": round(tot / args.steps, 4), "launches": cnt,
+                          "avg_launch_ms": tot / cnt, "achieved": wb / (tot / cnt * 1e-3) / 1e9,
+                          "unit": "GB/s", "work_per_launch": wb}
+    d = kern["hits_mask"]
+    value = (image_bytes + 12 * n_hits) / (ms_step * 1e-3) / 1e9
+    log(f"[bench] find_hits thr {thr}: {n_hits} hits, {ms_step * 1e3:.1f} us/step, "
+        f"{value:.0f} GB/s over the whole call")
+    out_json = {
+        "metric": "event hit finding: image bytes scanned + hits written per second",
+        "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "step_ms": {"median": round(float(np.median(per_step)), 4),
+                    "min": round(float(per_step.min()), 4), "max": round(float(per_step.max()), 4)},
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
+                               f"hits = ticks above {thr} that are local maxima along the wire, "
+                               "one pointid_find_hits call", "threshold": thr,
+                   "hits_found": n_hits, "image_bytes": image_bytes},
+        "roofline": {"kernel": "hits_mask", "bound": "hbm", "achieved": round(d["achieved"], 2),
+                     "peak": PEAK["hbm"], "unit": "GB/s",
+                     "frac": round(d["achieved"] / PEAK["hbm"], 4),
+                     "traffic": load_traffic("hits_mask", "config3_hits"),
+                     "avg_launch_ms": round(d["avg_launch_ms"], 4),
+                     "work_per_launch": d["work_per_launch"]},
+        "kernels": {k: {"ms_per_step": v["ms_per_step"], "launches": v["launches"],
+                        "achieved": round(v["achieved"], 2), "unit": "GB/s"}
+                    for k, v in kern.items()},
+    }
+    if not args.no_cpu_baseline:
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            cores = 1
+        t0 = time.perf_counter()
+        ref = oracle.find_hits(imgs_np, thr)
+        dt = time.perf_counter() - t0
+        out_json["cpu_baseline"] = {"value": round((image_bytes + 12 * len(ref)) / dt / 1e9, 3),
+                                    "unit": "GB/s", "cores": 1, "kind": "oracle",
+                                    "sample": f"the whole event, oracle.find_hits (numpy, one "
+                                              f"thread; {cores} BLAS threads unused); {dt:.2f} s",
+                                    "seconds": round(dt, 2)}
+        got = out[:min(n_hits, cap)].cpu().numpy()
+        out_json["matches_oracle"] = bool(len(ref) == n_hits and np.array_equal(got, ref))
+    h.close()
+    print(json.dumps(out_json), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -363,6 +461,11 @@ def main():
         del src, dst
     if args.config == 5:
         serving(args, torch, pid, synth)
+        return
+    if args.find_hits is not None:
+        if args.config != 3:
+            raise SystemExit("--find-hits runs on the config 3 event planes")
+        hit_finding(args, torch, pid, synth)
         return
     log(f"[bench] building config {args.config} workload")
     step, n, desc, sample, footprint, hit_bytes = make_workload(args, torch, pid)

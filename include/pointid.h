@@ -248,6 +248,35 @@ int pointid_gather_planes(const pointid_plane *planes, int32_t n_planes,
                           void *patches_out, int out_dtype, void *stream);
 
 /*
+ * Hit finding on deconvolved plane images (paper §2.1: wire hits, with their
+ * peak time, are found on the deconvolved waveforms before they are
+ * classified; the paper names no algorithm).  Reading used here: tick t of a
+ * wire's waveform x is a hit when x[t] > threshold, x[t] > x[t-1] and
+ * x[t] >= x[t+1], ticks outside the waveform counting as minus infinity (a
+ * plateau gives one hit, at its first tick).  The comparisons are exact fp32
+ * comparisons, so the result is bit-exact and deterministic.
+ *   planes     HOST array of n_planes descriptors (1 <= n_planes <= 64), read
+ *              during the call only; any image alignment
+ *   threshold  fp32 (a NaN threshold finds no hit)
+ *   hits_out   device int32 [capacity][3] = (plane, wire, tick), in plane, then
+ *              wire, then tick order -- the input layout of
+ *              pointid_classify_planes; the first min(found, capacity) hits
+ *              are written, the rest of the buffer is left as it was
+ *   capacity   >= 0; hits_out may be NULL when it is 0
+ *   n_found    device int64, 8-byte aligned: receives the number of hits
+ *              found, which may exceed capacity (then call again with a larger
+ *              buffer); read it after the stream has passed the call
+ * Uses the handle's device and scratch cache (about image bytes / 32 of
+ * scratch); the network weights are not used.
+ * Errors: EINVAL (NULL handle, planes or n_found; misaligned n_found;
+ * capacity < 0; NULL hits_out with capacity > 0; a bad plane as in
+ * pointid_classify_planes), ENOMEM, EHIP.
+ */
+int pointid_find_hits(pointid_handle h, const pointid_plane *planes,
+                      int32_t n_planes, float threshold, int32_t *hits_out,
+                      int64_t capacity, int64_t *n_found, void *stream);
+
+/*
  * Kernel timing for measurement tools (not needed for classification).  While
  * enabled (process-wide), every kernel this library launches is bracketed by
  * two HIP events recorded on the stream the kernel runs on.

@@ -81,6 +81,8 @@ def _load():
         "pointid_batcher_wait": (cint, [vp, ctypes.c_uint64]),
         "pointid_gather": (cint, [vp, i32, i32, vp, i64, vp, cint, vp]),
         "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
+        "pointid_find_hits": (cint, [vp, ctypes.POINTER(_Plane), i32, ctypes.c_float, vp, i64,
+                                     vp, vp]),
         "pointid_timing_enable": (cint, [cint]),
         "pointid_timing_reset": (cint, []),
         "pointid_timing_query": (cint, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -101,7 +103,7 @@ EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_c
             "pointid_batcher_create", "pointid_batcher_destroy", "pointid_batcher_submit",
             "pointid_batcher_wait",
             "pointid_gather",
-            "pointid_gather_planes", "pointid_timing_enable", "pointid_timing_reset",
+            "pointid_gather_planes", "pointid_find_hits", "pointid_timing_enable", "pointid_timing_reset",
             "pointid_timing_query", "pointid_last_error", "pointid_version")
 
 
@@ -372,3 +374,31 @@ def pointid_gather_planes(images, hits: torch.Tensor, out_dtype="fp32",
     _check(lib.pointid_gather_planes(arr, len(images), _ptr(hits), n, _ptr(out), code,
                                      _stream_ptr(stream, hits.device)))
     return out
+
+
+def pointid_find_hits(h: Handle, images, threshold: float, capacity: int | None = None,
+                      hits_out: torch.Tensor | None = None, n_found: torch.Tensor | None = None,
+                      stream=None):
+    """Hits (plane, wire, tick) of fp32 plane images, found on the device.
+
+    Returns ``(hits_out, n_found)``: int32 [capacity][3], of which the first
+    min(n_found, capacity) rows are written, and a device int64 [1] holding the
+    number of hits found (read it after the stream has passed the call).
+    ``capacity`` defaults to ``hits_out``'s length, else to 65,536.
+    """
+    arr = _plane_array(images)
+    dev = images[0].device
+    if hits_out is None:
+        cap = 65536 if capacity is None else int(capacity)
+        hits_out = torch.empty((cap, 3), dtype=torch.int32, device=dev)
+    _need(hits_out, torch.int32, "hits_out", h.device, (3,))
+    cap = hits_out.shape[0] if capacity is None else int(capacity)
+    if cap > hits_out.shape[0]:
+        raise ValueError("capacity exceeds hits_out")
+    if n_found is None:
+        n_found = torch.empty((1,), dtype=torch.int64, device=dev)
+    _need(n_found, torch.int64, "n_found", h.device)
+    _check(lib.pointid_find_hits(h.raw, arr, len(images), float(threshold),
+                                 _ptr(hits_out) if cap > 0 else ctypes.c_void_p(0), cap,
+                                 _ptr(n_found), _stream_ptr(stream, dev)))
+    return hits_out, n_found

@@ -21,8 +21,8 @@ OBJDIR = os.path.join(CSRC, "_build")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpointid.so")
 
-SOURCES = ["api.hip", "batcher.hip", "gather.hip", "fp32_mfma.hip", "conv_fc1_16.hip", "pack.hip",
-           "tail.hip"]
+SOURCES = ["api.hip", "batcher.hip", "gather.hip", "fp32_mfma.hip", "conv_fc1_16.hip", "hits.hip",
+           "pack.hip", "tail.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

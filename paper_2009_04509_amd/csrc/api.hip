@@ -674,4 +674,56 @@ int pointid_gather_planes(const pointid_plane* planes, int32_t n_planes, const i
   return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
 }
 
+
+int pointid_find_hits(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
+                      float threshold, int32_t* hits_out, int64_t capacity, int64_t* n_found,
+                      void* stream_) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (capacity < 0) return fail(POINTID_EINVAL, "capacity is negative");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (!n_found) return fail(POINTID_EINVAL, "n_found is NULL");
+  if ((reinterpret_cast<uintptr_t>(n_found) & 7) != 0)
+    return fail(POINTID_EINVAL, "n_found must be 8-byte aligned");
+  if (capacity > 0 && !hits_out) return fail(POINTID_EINVAL, "hits_out is NULL");
+  HitRows rows;
+  std::memset(&rows, 0, sizeof(rows));
+  hit_rows(t, &rows);
+  const int64_t n_rows = rows.row0[rows.n];
+  const int64_t stride = hits_mask_stride(t);
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  const size_t mask_bytes = sizeof(uint64_t) * (size_t)n_rows * (size_t)stride;
+  const size_t count_bytes = sizeof(int32_t) * (size_t)n_rows;
+  const size_t off_bytes = sizeof(int64_t) * (size_t)n_rows;
+  Workspace ws(h->scratch, stream);
+  hipError_t e = ws.reserve(pad256(mask_bytes) + pad256(count_bytes) + pad256(off_bytes));
+  if (e != hipSuccess) return hip_fail(e, "scratch buffer");
+  uint64_t* mask = nullptr;
+  int32_t* counts = nullptr;
+  int64_t* offsets = nullptr;
+  e = ws.get(mask_bytes, (void**)&mask);
+  if (e == hipSuccess) e = ws.get(count_bytes, (void**)&counts);
+  if (e == hipSuccess) e = ws.get(off_bytes, (void**)&offsets);
+  if (e != hipSuccess) return hip_fail(e, "workspace (hit finding)");
+  {
+    KernelTimer kt("hits_mask", stream);
+    e = launch_hits_mask(t, rows, threshold, mask, stride, counts, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "hit mask launch");
+  {
+    KernelTimer kt("hits_scan", stream);
+    e = launch_hits_scan(counts, n_rows, offsets, n_found, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "hit scan launch");
+  {
+    KernelTimer kt("hits_emit", stream);
+    e = launch_hits_emit(rows, mask, stride, counts, offsets, hits_out, capacity, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "hit emit launch");
+  return POINTID_OK;
+}
+
 }  // extern "C"

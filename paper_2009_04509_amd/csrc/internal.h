@@ -130,4 +130,26 @@ hipError_t launch_tail(const float* part, int splits, int64_t n,
 hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
                                 const RequestTable& reqs, hipStream_t stream);
 
+// Hit finding (hits.hip): rows are the wires of all planes in plane order;
+// row0[p] is plane p's first row, row0[n] the row count.
+struct HitRows {
+  int64_t row0[kMaxPlanes + 1];
+  int32_t n_ticks[kMaxPlanes];
+  int32_t n;
+};
+void hit_rows(const PlaneTable& planes, HitRows* rows);
+// uint64 words of hit bits per row (4 per 256 ticks of the longest plane).
+int64_t hits_mask_stride(const PlaneTable& planes);
+// Row r's hit bits into mask[r * mask_stride ...] and its hit count into counts[r].
+hipError_t launch_hits_mask(const PlaneTable& planes, const HitRows& rows, float threshold,
+                            uint64_t* mask, int64_t mask_stride, int32_t* counts,
+                            hipStream_t stream);
+// offsets[r] = sum of counts[0 .. r-1]; *total = sum of all counts.
+hipError_t launch_hits_scan(const int32_t* counts, int64_t n_rows, int64_t* offsets,
+                            int64_t* total, hipStream_t stream);
+// (plane, wire, tick) of every hit with output index below `capacity`.
+hipError_t launch_hits_emit(const HitRows& rows, const uint64_t* mask, int64_t mask_stride,
+                            const int32_t* counts, const int64_t* offsets, int32_t* hits,
+                            int64_t capacity, hipStream_t stream);
+
 }  // namespace pointid

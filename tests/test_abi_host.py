@@ -165,3 +165,24 @@ def test_binding_shape_checks(b):
                           "fc2_b": np.zeros(5, np.float32)})
     with pytest.raises((TypeError, ValueError)):
         b.pointid_gather(torch.zeros(4, 4), torch.zeros(3, 2, dtype=torch.int32))
+
+
+def test_find_hits_validation(b):
+    L = b.lib
+    P = b._Plane
+    good = (P * 1)(P(0x1000, 10, 10))
+    n_found = ctypes.c_void_p(0x2000)
+    assert L.pointid_find_hits(NULL, good, 1, 1.0, FAKE, 5, n_found, NULL) == b.POINTID_EINVAL
+    assert "handle" in b.pointid_last_error()
+    # handle checks come first; the remaining rules are exercised with a fake
+    # non-NULL handle that validation rejects before it is ever used
+    H = ctypes.c_void_p(0x3000)
+    assert L.pointid_find_hits(H, good, 1, 1.0, FAKE, -1, n_found, NULL) == b.POINTID_EINVAL
+    assert "capacity" in b.pointid_last_error()
+    assert L.pointid_find_hits(H, good, 0, 1.0, FAKE, 5, n_found, NULL) == b.POINTID_EINVAL
+    assert L.pointid_find_hits(H, None, 1, 1.0, FAKE, 5, n_found, NULL) == b.POINTID_EINVAL
+    assert L.pointid_find_hits(H, good, 1, 1.0, FAKE, 5, NULL, NULL) == b.POINTID_EINVAL
+    assert L.pointid_find_hits(H, good, 1, 1.0, FAKE, 5, ctypes.c_void_p(0x2004), NULL) == b.POINTID_EINVAL
+    assert "aligned" in b.pointid_last_error()
+    assert L.pointid_find_hits(H, good, 1, 1.0, NULL, 5, n_found, NULL) == b.POINTID_EINVAL
+    assert "hits_out" in b.pointid_last_error()
