@@ -687,17 +687,15 @@ int pointid_find_hits(pointid_handle h, const pointid_plane* planes, int32_t n_p
   if ((reinterpret_cast<uintptr_t>(n_found) & 7) != 0)
     return fail(POINTID_EINVAL, "n_found must be 8-byte aligned");
   if (capacity > 0 && !hits_out) return fail(POINTID_EINVAL, "hits_out is NULL");
-  HitRows rows;
-  std::memset(&rows, 0, sizeof(rows));
-  hit_rows(t, &rows);
-  const int64_t n_rows = rows.row0[rows.n];
-  const int64_t stride = hits_mask_stride(t);
+  HitSteps st;
+  std::memset(&st, 0, sizeof(st));
+  hit_steps(t, &st);
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
-  const size_t mask_bytes = sizeof(uint64_t) * (size_t)n_rows * (size_t)stride;
-  const size_t count_bytes = sizeof(int32_t) * (size_t)n_rows;
-  const size_t off_bytes = sizeof(int64_t) * (size_t)n_rows;
+  const size_t mask_bytes = 4 * sizeof(uint64_t) * (size_t)st.step0[st.n];
+  const size_t count_bytes = sizeof(int32_t) * (size_t)st.workers;
+  const size_t off_bytes = sizeof(int64_t) * (size_t)st.workers;
   Workspace ws(h->scratch, stream);
   hipError_t e = ws.reserve(pad256(mask_bytes) + pad256(count_bytes) + pad256(off_bytes));
   if (e != hipSuccess) return hip_fail(e, "scratch buffer");
@@ -710,17 +708,17 @@ int pointid_find_hits(pointid_handle h, const pointid_plane* planes, int32_t n_p
   if (e != hipSuccess) return hip_fail(e, "workspace (hit finding)");
   {
     KernelTimer kt("hits_mask", stream);
-    e = launch_hits_mask(t, rows, threshold, mask, stride, counts, stream);
+    e = launch_hits_mask(t, st, threshold, mask, counts, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "hit mask launch");
   {
     KernelTimer kt("hits_scan", stream);
-    e = launch_hits_scan(counts, n_rows, offsets, n_found, stream);
+    e = launch_hits_scan(counts, st.workers, offsets, n_found, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "hit scan launch");
   {
     KernelTimer kt("hits_emit", stream);
-    e = launch_hits_emit(rows, mask, stride, counts, offsets, hits_out, capacity, stream);
+    e = launch_hits_emit(t, st, mask, counts, offsets, hits_out, capacity, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "hit emit launch");
   return POINTID_OK;

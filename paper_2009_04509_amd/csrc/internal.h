@@ -130,25 +130,31 @@ hipError_t launch_tail(const float* part, int splits, int64_t n,
 hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
                                 const RequestTable& reqs, hipStream_t stream);
 
-// Hit finding (hits.hip): rows are the wires of all planes in plane order;
-// row0[p] is plane p's first row, row0[n] the row count.
-struct HitRows {
-  int64_t row0[kMaxPlanes + 1];
-  int32_t n_ticks[kMaxPlanes];
+// Hit finding (hits.hip).  The waveforms of all planes are cut into steps of
+// 256 ticks, numbered plane by plane, wire by wire, then along the wire; step
+// g covers ticks 256*s .. 256*s + 255 of one wire.  Each of `workers` waves
+// takes the steps [w * per, min((w + 1) * per, total)).
+constexpr int kHitStep = 256;
+constexpr int kHitMaxWorkers = 8192;
+struct HitSteps {
+  int64_t step0[kMaxPlanes + 1];    // first step of plane p; step0[n] = total
+  int32_t per_row[kMaxPlanes];      // steps per wire of plane p
+  int64_t per;                      // steps per worker
+  int32_t workers;
   int32_t n;
 };
-void hit_rows(const PlaneTable& planes, HitRows* rows);
-// uint64 words of hit bits per row (4 per 256 ticks of the longest plane).
-int64_t hits_mask_stride(const PlaneTable& planes);
-// Row r's hit bits into mask[r * mask_stride ...] and its hit count into counts[r].
-hipError_t launch_hits_mask(const PlaneTable& planes, const HitRows& rows, float threshold,
-                            uint64_t* mask, int64_t mask_stride, int32_t* counts,
+void hit_steps(const PlaneTable& planes, HitSteps* st);
+// Every step's hit bits (4 uint64 words: bit l of word j = tick 4l + j of the
+// step) into mask[4g ...]; each worker's hit count into counts[w].  kVec
+// (every image 16-byte aligned, every n_ticks a multiple of 4) allows 16-byte
+// loads.
+hipError_t launch_hits_mask(const PlaneTable& planes, const HitSteps& st, float threshold,
+                            uint64_t* mask, int32_t* counts, hipStream_t stream);
+// offsets[w] = sum of counts[0 .. w-1]; *total = sum of all counts.
+hipError_t launch_hits_scan(const int32_t* counts, int32_t n, int64_t* offsets, int64_t* total,
                             hipStream_t stream);
-// offsets[r] = sum of counts[0 .. r-1]; *total = sum of all counts.
-hipError_t launch_hits_scan(const int32_t* counts, int64_t n_rows, int64_t* offsets,
-                            int64_t* total, hipStream_t stream);
 // (plane, wire, tick) of every hit with output index below `capacity`.
-hipError_t launch_hits_emit(const HitRows& rows, const uint64_t* mask, int64_t mask_stride,
+hipError_t launch_hits_emit(const PlaneTable& planes, const HitSteps& st, const uint64_t* mask,
                             const int32_t* counts, const int64_t* offsets, int32_t* hits,
                             int64_t capacity, hipStream_t stream);
 

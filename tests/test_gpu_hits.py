@@ -78,6 +78,21 @@ def test_gaussian_planes_and_odd_lengths(pid, handle):
         check_exact(pid, handle, imgs, thr)
 
 
+def test_worker_ranges_cross_wires_and_planes(pid, handle):
+    # enough 256-tick steps that every wave owns several, so its range starts
+    # and ends mid-wire and crosses wires and planes; odd lengths (4-byte loads)
+    # and multiples of 4 (16-byte loads)
+    rng = np.random.default_rng(17)
+    odd = [rng.integers(-3, 6, size=s).astype(np.float32)
+           for s in [(700, 6001), (500, 777), (900, 2000)]]
+    even = [rng.integers(-3, 6, size=s).astype(np.float32) for s in [(4000, 1028), (37, 6000)]]
+    say("find_hits long worker ranges")
+    for imgs in (odd, even):
+        steps = sum(a.shape[0] * -(-a.shape[1] // 256) for a in imgs)
+        assert steps > 2 * 8192
+        check_exact(pid, handle, imgs, 2.0)
+
+
 def test_unaligned_image_base(pid, handle):
     rng = np.random.default_rng(13)
     W, T = 21, 700                                  # T % 4 == 0, base off by 4 bytes
