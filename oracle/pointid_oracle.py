@@ -20,6 +20,16 @@ What it computes, with the passage each step follows:
   has a bias (the paper's parameter count of 11,900,420 requires all six), and
   the 44x44x48 maps are flattened channels-last, index (y*44 + x)*48 + k.
 
+* Time-interval columns, paper §2.1: each pixel holds the charge that the
+  deconvolved waveform of its wire deposits in the time interval of its column.
+  With one tick per column this is the plane pixel itself (the reading above).
+  Reading used for D ticks per column: the waveform is binned once into
+  columns of D ticks aligned to tick 0, column j covering ticks jD .. jD + D - 1
+  (the last column of a plane only the ticks that exist), and a column's value
+  is the sum of its samples (the charge in the interval); the patch of hit
+  (w, t) is then cut from the binned plane around column floor(t / D), with
+  the same centring and zero fill as above.
+
 * Hit finding, paper §2.1: the reconstruction finds wire hits on the
   deconvolved waveforms (giving peak time and charge) before they are
   classified; the paper names no algorithm.  Reading used here: a hit is a tick
@@ -92,6 +102,38 @@ def gather_patches_planes(images, hits3) -> np.ndarray:
         if sel.size:
             out[sel] = gather_patches(img, hits3[sel, 1:3])
     return out
+
+
+# --------------------------------------------------------------------------
+# Columns of D ticks (paper §2.1; the reading is in the module docstring)
+# --------------------------------------------------------------------------
+
+def downsample_plane(image, ticks_per_column) -> np.ndarray:
+    """float32 [n_wires][ceil(n_ticks / D)]: column j is the sum of ticks
+    jD .. jD + D - 1 that exist, summed in float64 and rounded once."""
+    D = int(ticks_per_column)
+    if D < 1:
+        raise ValueError("ticks_per_column must be >= 1")
+    x = np.asarray(image, dtype=np.float32).astype(np.float64)
+    W, T = x.shape
+    J = -(-T // D)
+    padded = np.zeros((W, J * D), np.float64)
+    padded[:, :T] = x
+    return padded.reshape(W, J, D).sum(axis=2).astype(np.float32)
+
+
+def hits_to_columns(hits3, ticks_per_column) -> np.ndarray:
+    """(plane, wire, column) of each hit: column = floor(tick / D)."""
+    h = np.array(hits3, dtype=np.int64).reshape(-1, 3)
+    h[:, 2] = np.floor_divide(h[:, 2], int(ticks_per_column))
+    return h
+
+
+def gather_patches_planes_ds(images, hits3, ticks_per_column) -> np.ndarray:
+    """Patches with D ticks per column: cut from the binned planes around the
+    hit's column."""
+    binned = [downsample_plane(img, ticks_per_column) for img in images]
+    return gather_patches_planes(binned, hits_to_columns(hits3, ticks_per_column))
 
 
 # --------------------------------------------------------------------------
@@ -260,6 +302,12 @@ def classify_planes(images, hits3, weights, chunk: int = CHUNK) -> np.ndarray:
         out[s:s + chunk] = forward(gather_patches_planes(images, hits3[s:s + chunk]),
                                    weights).astype(np.float32)
     return out
+
+
+def classify_planes_ds(images, hits3, weights, ticks_per_column, chunk: int = CHUNK) -> np.ndarray:
+    """Scores of hits (plane, wire, tick) with patches of D ticks per column."""
+    binned = [downsample_plane(img, ticks_per_column) for img in images]
+    return classify_planes(binned, hits_to_columns(hits3, ticks_per_column), weights, chunk)
 
 
 def quantize_16bit_model(weights, kind: str = "bf16") -> dict:

@@ -392,3 +392,84 @@ def test_hit_finding_single_pulse_and_order():
     got = oracle.find_hits([a, b], 1.0)
     assert got.tolist() == [[0, 0, 20], [0, 1, 150], [0, 2, 77], [1, 1, 5], [1, 1, 190]]
     assert oracle.find_hits([b], 9.0).shape == (0, 3)       # equal to the threshold
+
+
+# ------------------------------------------------------- columns of D ticks
+
+def test_downsample_worked_cases():
+    row = np.array([[1, 2, 3, 4, 5, 6, 7]], np.float32)
+    assert oracle.downsample_plane(row, 3).tolist() == [[6, 15, 7]]      # ragged last column
+    assert oracle.downsample_plane(row, 7).tolist() == [[28]]
+    assert oracle.downsample_plane(row, 10).tolist() == [[28]]
+    assert oracle.downsample_plane(row, 2).tolist() == [[3, 7, 11, 7]]
+    assert np.array_equal(oracle.downsample_plane(row, 1), row)         # one tick per column
+    with pytest.raises(ValueError):
+        oracle.downsample_plane(row, 0)
+
+
+def test_downsample_one_tick_is_the_plain_gather():
+    rng = np.random.default_rng(21)
+    imgs = [rng.normal(0, 2.5, size=(60, 300)).astype(np.float32),
+            rng.normal(0, 2.5, size=(30, 77)).astype(np.float32)]
+    hits = np.c_[rng.integers(0, 2, 200), rng.integers(-30, 90, 200), rng.integers(-40, 340, 200)]
+    assert np.array_equal(oracle.gather_patches_planes_ds(imgs, hits, 1),
+                          oracle.gather_patches_planes(imgs, hits))
+
+
+def test_downsample_coordinate_image_closed_form():
+    # I[w][t] = 1 + 1000 w + t: a full column j of D ticks sums to
+    # D (1 + 1000 w + D j) + D (D - 1) / 2, exactly
+    W, T, D = 100, 500, 4
+    img = synth.coord_image(W, T)
+    ds = oracle.downsample_plane(img, D)
+    assert ds.shape == (W, 125)
+    w, j = np.meshgrid(np.arange(W), np.arange(125), indexing="ij")
+    assert np.array_equal(ds, (D * (1 + 1000 * w + D * j) + D * (D - 1) // 2).astype(np.float32))
+    # hit (plane 0, wire 50, tick 203) -> column 50; patch (r, c) is binned
+    # pixel (26 + r, 26 + c), all inside the plane
+    P = oracle.gather_patches_planes_ds([img], [[0, 50, 203]], D)[0]
+    r, c = np.meshgrid(np.arange(48), np.arange(48), indexing="ij")
+    want = D * (1 + 1000 * (26 + r) + D * (26 + c)) + 6
+    assert np.array_equal(P, want.astype(np.float32))
+    # ticks 200..203 all give column 50; tick 204 gives column 51
+    for t in (200, 201, 202):
+        assert np.array_equal(oracle.gather_patches_planes_ds([img], [[0, 50, t]], D)[0], P)
+    assert not np.array_equal(oracle.gather_patches_planes_ds([img], [[0, 50, 204]], D)[0], P)
+
+
+def test_downsample_negative_tick_and_edges():
+    # floor division: tick -5 with D = 4 is column -2, so patch column c holds
+    # binned column c - 26 and columns c < 26 are zero
+    W, T, D = 10, 30, 4
+    img = synth.coord_image(W, T)
+    ds = oracle.downsample_plane(img, D)                     # 8 columns, the last of 2 ticks
+    assert ds[3, 7] == (1 + 3000 + 28) + (1 + 3000 + 29)
+    P = oracle.gather_patches_planes_ds([img], [[0, 3, -5]], D)[0]
+    assert (P[:, :26] == 0).all()
+    assert P[24, 26] == ds[3, 0] and P[24, 33] == ds[3, 7]
+    assert (P[:, 34:] == 0).all()                            # past the 8 columns
+    assert (P[:21, :] == 0).all() and (P[31:, :] == 0).all()  # wires outside 0..9
+
+
+def test_downsample_bruteforce_and_charge_conservation():
+    rng = np.random.default_rng(22)
+    imgs = [rng.normal(0, 2.5, size=(9, 61)).astype(np.float32),
+            rng.normal(5, 2.5, size=(4, 13)).astype(np.float32)]
+    D = 6
+    hits = np.c_[rng.integers(-1, 3, 40), rng.integers(-3, 12, 40), rng.integers(-20, 80, 40)]
+    got = oracle.gather_patches_planes_ds(imgs, hits, D)
+    for i, (p, w, t) in enumerate(hits):
+        for r in range(48):
+            for c in range(48):
+                v = 0.0
+                if 0 <= p < len(imgs):
+                    img = imgs[p]
+                    ww = w - 24 + r
+                    col = t // D - 24 + c                    # Python // is floor division
+                    if 0 <= ww < img.shape[0] and col >= 0:
+                        ticks = [tt for tt in range(col * D, col * D + D) if tt < img.shape[1]]
+                        v = float(np.float32(sum(float(img[ww, tt]) for tt in ticks)))
+                assert got[i, r, c] == np.float32(v), (i, r, c)
+    for img in imgs:                                         # the binning keeps the charge
+        assert abs(oracle.downsample_plane(img, D).astype(np.float64).sum()
+                   - img.astype(np.float64).sum()) < 1e-4
