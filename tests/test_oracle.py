@@ -398,10 +398,11 @@ def test_hit_finding_single_pulse_and_order():
 
 def test_downsample_worked_cases():
     row = np.array([[1, 2, 3, 4, 5, 6, 7]], np.float32)
-    assert oracle.downsample_plane(row, 3).tolist() == [[6, 15, 7]]      # ragged last column
-    assert oracle.downsample_plane(row, 7).tolist() == [[28]]
-    assert oracle.downsample_plane(row, 10).tolist() == [[28]]
-    assert oracle.downsample_plane(row, 2).tolist() == [[3, 7, 11, 7]]
+    # ragged last column: its missing ticks count as 0
+    assert np.array_equal(oracle.downsample_plane(row, 3), np.float32([[2, 5, 7 / 3]]))
+    assert oracle.downsample_plane(row, 7).tolist() == [[4]]
+    assert np.array_equal(oracle.downsample_plane(row, 10), np.float32([[2.8]]))
+    assert oracle.downsample_plane(row, 2).tolist() == [[1.5, 3.5, 5.5, 3.5]]
     assert np.array_equal(oracle.downsample_plane(row, 1), row)         # one tick per column
     with pytest.raises(ValueError):
         oracle.downsample_plane(row, 0)
@@ -417,19 +418,19 @@ def test_downsample_one_tick_is_the_plain_gather():
 
 
 def test_downsample_coordinate_image_closed_form():
-    # I[w][t] = 1 + 1000 w + t: a full column j of D ticks sums to
-    # D (1 + 1000 w + D j) + D (D - 1) / 2, exactly
+    # I[w][t] = 1 + 1000 w + t: a full column j of D ticks averages
+    # 1 + 1000 w + D j + (D - 1) / 2, exactly
     W, T, D = 100, 500, 4
     img = synth.coord_image(W, T)
     ds = oracle.downsample_plane(img, D)
     assert ds.shape == (W, 125)
     w, j = np.meshgrid(np.arange(W), np.arange(125), indexing="ij")
-    assert np.array_equal(ds, (D * (1 + 1000 * w + D * j) + D * (D - 1) // 2).astype(np.float32))
+    assert np.array_equal(ds, (1 + 1000 * w + D * j + (D - 1) / 2).astype(np.float32))
     # hit (plane 0, wire 50, tick 203) -> column 50; patch (r, c) is binned
     # pixel (26 + r, 26 + c), all inside the plane
     P = oracle.gather_patches_planes_ds([img], [[0, 50, 203]], D)[0]
     r, c = np.meshgrid(np.arange(48), np.arange(48), indexing="ij")
-    want = D * (1 + 1000 * (26 + r) + D * (26 + c)) + 6
+    want = 1 + 1000 * (26 + r) + D * (26 + c) + 1.5
     assert np.array_equal(P, want.astype(np.float32))
     # ticks 200..203 all give column 50; tick 204 gives column 51
     for t in (200, 201, 202):
@@ -443,7 +444,7 @@ def test_downsample_negative_tick_and_edges():
     W, T, D = 10, 30, 4
     img = synth.coord_image(W, T)
     ds = oracle.downsample_plane(img, D)                     # 8 columns, the last of 2 ticks
-    assert ds[3, 7] == (1 + 3000 + 28) + (1 + 3000 + 29)
+    assert ds[3, 7] == ((1 + 3000 + 28) + (1 + 3000 + 29)) / 4
     P = oracle.gather_patches_planes_ds([img], [[0, 3, -5]], D)[0]
     assert (P[:, :26] == 0).all()
     assert P[24, 26] == ds[3, 0] and P[24, 33] == ds[3, 7]
@@ -468,8 +469,8 @@ def test_downsample_bruteforce_and_charge_conservation():
                     col = t // D - 24 + c                    # Python // is floor division
                     if 0 <= ww < img.shape[0] and col >= 0:
                         ticks = [tt for tt in range(col * D, col * D + D) if tt < img.shape[1]]
-                        v = float(np.float32(sum(float(img[ww, tt]) for tt in ticks)))
+                        v = float(np.float32(sum(float(img[ww, tt]) for tt in ticks) / D))
                 assert got[i, r, c] == np.float32(v), (i, r, c)
     for img in imgs:                                         # the binning keeps the charge
-        assert abs(oracle.downsample_plane(img, D).astype(np.float64).sum()
+        assert abs(D * oracle.downsample_plane(img, D).astype(np.float64).sum()
                    - img.astype(np.float64).sum()) < 1e-4
