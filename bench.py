@@ -47,6 +47,7 @@ KERNELS = {
     "fc1_fp32": ("flops_fc1", "fp32_mfma.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
     "tail": ("bytes_tail", "tail.hip"),
+    "bin_ticks": ("bytes_bin", "gather.hip"),
     "hits_mask": ("bytes_hits_mask", "hits.hip"),
     "hits_scan": ("bytes_hits_scan", "hits.hip"),
     "hits_emit": ("bytes_hits_emit", "hits.hip"),
@@ -78,6 +79,9 @@ def parse():
                          "through the dynamic batcher when --batch-requests K > 0)")
     ap.add_argument("--batch-delay-us", type=int, default=200,
                     help="config 5 with --clients: the batcher's longest wait for a fuller batch")
+    ap.add_argument("--ticks-per-column", type=int, default=1, metavar="D",
+                    help="config 3: patches whose columns span D ticks "
+                         "(pointid_classify_planes_ds; 1 = pointid_classify_planes)")
     ap.add_argument("--find-hits", type=float, default=None, metavar="THR",
                     help="config 3: time hit finding (pointid_find_hits) on the event's 18 "
                          "planes at threshold THR instead of classification")
@@ -122,15 +126,30 @@ def make_workload(args, torch, pid):
         hits = torch.from_numpy(h3).to(dev)
         n = len(h3)
         scores = torch.empty((n, 4), dtype=torch.float32, device=dev)
-        footprint = _footprint([p.image.shape for p in planes], h3)
+        D = args.ticks_per_column
+        if D > 1:
+            shapes = [(p.image.shape[0], -(-p.image.shape[1] // D)) for p in planes]
+            cols = h3.copy()
+            cols[:, 2] = np.floor_divide(cols[:, 2], D)
+            footprint = _footprint(shapes, cols)
 
-        def step(h):
-            pid.pointid_classify_planes(h, imgs, hits, scores)
+            def step(h):
+                pid.pointid_classify_planes_ds(h, imgs, hits, D, scores)
 
-        desc = {"workload": "event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
-                            "50,000 hits, one pointid_classify_planes call",
-                "hits": n, "planes": 18, "ticks": 6000}
-        sample = dict(kind="planes", images=[p.image for p in planes], hits=h3)
+            desc = {"workload": f"event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
+                                f"50,000 hits, patch columns of {D} ticks, one "
+                                "pointid_classify_planes_ds call (binning included)",
+                    "hits": n, "planes": 18, "ticks": 6000, "ticks_per_column": D}
+        else:
+            footprint = _footprint([p.image.shape for p in planes], h3)
+
+            def step(h):
+                pid.pointid_classify_planes(h, imgs, hits, scores)
+
+            desc = {"workload": "event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
+                                "50,000 hits, one pointid_classify_planes call",
+                    "hits": n, "planes": 18, "ticks": 6000}
+        sample = dict(kind="planes", images=[p.image for p in planes], hits=h3, D=D)
         hit_bytes = 12
     elif args.config == 2:
         p = synth.config2()
@@ -192,8 +211,13 @@ def cpu_baseline(sample, n_sample):
     if sample["kind"] == "planes":
         idx = np.sort(rng.choice(len(sample["hits"]), n_sample, replace=False))
         t0 = time.perf_counter()
-        oracle.classify_planes(sample["images"], sample["hits"][idx], w)
-        what = f"{n_sample} hits sampled (seeded) from the 50,000-hit event, oracle.classify_planes"
+        if sample.get("D", 1) > 1:
+            oracle.classify_planes_ds(sample["images"], sample["hits"][idx], w, sample["D"])
+            what = (f"{n_sample} hits sampled (seeded) from the 50,000-hit event, "
+                    f"oracle.classify_planes_ds with D = {sample['D']} (binning included)")
+        else:
+            oracle.classify_planes(sample["images"], sample["hits"][idx], w)
+            what = f"{n_sample} hits sampled (seeded) from the 50,000-hit event, oracle.classify_planes"
     elif sample["kind"] == "plane":
         idx = np.sort(rng.choice(len(sample["hits"]), min(n_sample, len(sample["hits"])), replace=False))
         t0 = time.perf_counter()
@@ -507,6 +531,10 @@ def main():
             unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
         elif model == "bytes_tail":
             work = args.steps * per_step_patches * (8 * 128 * 4 + 16)
+            unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
+        elif model == "bytes_bin":
+            img_bytes = 4 * 12480 * 6000
+            work = args.steps * (img_bytes + img_bytes // args.ticks_per_column)
             unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
         elif model == "bytes_cast":
             work = args.steps * per_step_patches * (9216 + 4608)

@@ -158,6 +158,27 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane *planes,
                             int32_t n_planes, const int32_t *hits,
                             int64_t n_hits, float *scores, void *stream);
 
+/*
+ * Classify hits with patches whose columns span D = ticks_per_column ticks
+ * each (paper §2.1: a pixel holds the charge its wire collects in the time
+ * interval of its column).  Each plane is binned once into columns of D ticks
+ * aligned to tick 0 -- column j holds the charge per tick of ticks
+ * jD .. jD + D - 1, their sum divided by D (ticks past the end of the plane
+ * count as 0), accumulated in fp64 and rounded to fp32 once -- and the patch of hit
+ * (plane, wire, tick) is cut from the binned plane around column
+ * floor(tick / D), exactly as pointid_classify_planes cuts it around a tick.
+ * D = 1 gives pointid_classify_planes' bits.
+ *   planes  HOST array of the unbinned planes, as in pointid_classify_planes
+ *   hits    device int32 [n_hits][3] = (plane, wire, tick), ticks unbinned
+ *   scores  device fp32 [n_hits][4], in hit order, 16-byte aligned
+ * The binned planes (image bytes / D) live in the handle's scratch cache.
+ * Errors as pointid_classify_planes, plus EINVAL for ticks_per_column < 1.
+ */
+int pointid_classify_planes_ds(pointid_handle h, const pointid_plane *planes,
+                               int32_t n_planes, int32_t ticks_per_column,
+                               const int32_t *hits, int64_t n_hits,
+                               float *scores, void *stream);
+
 /* One request of a batched call. */
 typedef struct {
     const int32_t *hits;   /* device int32: [n_hits][2] = (wire, tick) on plane
@@ -246,6 +267,20 @@ int pointid_gather(const float *image, int32_t n_wires, int32_t n_ticks,
 int pointid_gather_planes(const pointid_plane *planes, int32_t n_planes,
                           const int32_t *hits, int64_t n_hits,
                           void *patches_out, int out_dtype, void *stream);
+
+/*
+ * One plane binned into columns of D = ticks_per_column ticks (the binning of
+ * pointid_classify_planes_ds, alone; needs no handle and runs on the current
+ * HIP device).
+ *   image  device fp32 [n_wires][n_ticks], any 4-byte alignment
+ *   out    device fp32 [n_wires][ceil(n_ticks / D)]: out[w][j] = (sum of
+ *          image[w][jD + k] over k < D with jD + k < n_ticks) / D, accumulated
+ *          in fp64 in tick order and rounded once
+ * Errors: EINVAL (n_wires or n_ticks <= 0, ticks_per_column < 1, NULL
+ * pointer), EHIP.
+ */
+int pointid_downsample(const float *image, int32_t n_wires, int32_t n_ticks,
+                       int32_t ticks_per_column, float *out, void *stream);
 
 /*
  * Hit finding on deconvolved plane images (paper §2.1: wire hits, with their

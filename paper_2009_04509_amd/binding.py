@@ -71,6 +71,9 @@ def _load():
         "pointid_classify": (cint, [vp, vp, i32, i32, vp, i64, vp, vp]),
         "pointid_classify_planes": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp, vp]),
         "pointid_classify_patches": (cint, [vp, vp, i64, vp, vp]),
+        "pointid_classify_planes_ds": (cint, [vp, ctypes.POINTER(_Plane), i32, i32, vp, i64, vp,
+                                              vp]),
+        "pointid_downsample": (cint, [vp, i32, i32, i32, vp, vp]),
         "pointid_classify_requests": (cint, [vp, ctypes.POINTER(_Plane), i32,
                                              ctypes.POINTER(_Request), i32, vp]),
         "pointid_batcher_create": (cint, [vp, ctypes.POINTER(_Plane), i32, i32, i32,
@@ -103,7 +106,8 @@ EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_c
             "pointid_batcher_create", "pointid_batcher_destroy", "pointid_batcher_submit",
             "pointid_batcher_wait",
             "pointid_gather",
-            "pointid_gather_planes", "pointid_find_hits", "pointid_timing_enable", "pointid_timing_reset",
+            "pointid_gather_planes", "pointid_find_hits", "pointid_classify_planes_ds",
+            "pointid_downsample", "pointid_timing_enable", "pointid_timing_reset",
             "pointid_timing_query", "pointid_last_error", "pointid_version")
 
 
@@ -256,6 +260,41 @@ def pointid_classify_planes(h: Handle, images, hits: torch.Tensor,
     _check(lib.pointid_classify_planes(h.raw, arr, len(images), _ptr(hits), n, _ptr(scores),
                                        _stream_ptr(stream, hits.device)))
     return scores
+
+
+def pointid_classify_planes_ds(h: Handle, images, hits: torch.Tensor, ticks_per_column: int,
+                               scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Scores with patches of ``ticks_per_column`` ticks per column; hits are
+    (plane, wire, tick) in unbinned ticks over the unbinned plane images."""
+    arr = _plane_array(images)
+    _need(hits, torch.int32, "hits", h.device, (3,))
+    n = hits.shape[0]
+    if scores is None:
+        scores = torch.empty((n, 4), dtype=torch.float32, device=hits.device)
+    _need(scores, torch.float32, "scores", h.device, (4,))
+    _check(lib.pointid_classify_planes_ds(h.raw, arr, len(images), int(ticks_per_column),
+                                          _ptr(hits), n, _ptr(scores),
+                                          _stream_ptr(stream, hits.device)))
+    return scores
+
+
+def pointid_downsample(image: torch.Tensor, ticks_per_column: int,
+                       out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """fp32 image [W][T] binned into [W][ceil(T / D)] columns of D ticks."""
+    _need(image, torch.float32, "image")
+    if image.dim() != 2:
+        raise ValueError("image must be [n_wires][n_ticks]")
+    D = int(ticks_per_column)
+    W, T = image.shape
+    J = -(-T // D) if D >= 1 else 0
+    if out is None:
+        out = torch.empty((W, max(J, 1)), dtype=torch.float32, device=image.device)
+    _need(out, torch.float32, "out")
+    if tuple(out.shape) != (W, J):
+        raise ValueError(f"out must be [{W}, {J}]")
+    _check(lib.pointid_downsample(_ptr(image), W, T, D, _ptr(out),
+                                  _stream_ptr(stream, image.device)))
+    return out
 
 
 def pointid_classify_requests(h: Handle, images, requests, stream=None):

@@ -293,7 +293,7 @@ int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* 
 }
 
 int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hits,
-                  int stride, int64_t n, float* scores, void* stream_) {
+                  int stride, int64_t n, float* scores, void* stream_, int tick_div = 1) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
@@ -306,7 +306,7 @@ int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hit
   if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
   {
     KernelTimer kt("gather", stream);
-    e = launch_gather(planes, hits, stride, n, patches, h->precision, stream);
+    e = launch_gather(planes, hits, stride, n, patches, h->precision, stream, tick_div);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
   if (half)
@@ -565,6 +565,46 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane* planes, int32
   return classify_hits(h, t, hits, 3, n_hits, scores, stream);
 }
 
+int pointid_classify_planes_ds(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
+                               int32_t ticks_per_column, const int32_t* hits, int64_t n_hits,
+                               float* scores, void* stream_) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  if (ticks_per_column < 1) return fail(POINTID_EINVAL, "ticks_per_column must be >= 1");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (n_hits == 0) return POINTID_OK;
+  if (!hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  // the binned planes live in a scratch buffer of their own until the
+  // classification below has been enqueued after the binning
+  PlaneTable binned = t;
+  size_t bytes = 0;
+  for (int i = 0; i < t.n; ++i) {
+    binned.p[i].n_ticks = (int32_t)(((int64_t)t.p[i].n_ticks + ticks_per_column - 1) / ticks_per_column);
+    bytes += pad256(sizeof(float) * (size_t)t.p[i].n_wires * (size_t)binned.p[i].n_ticks);
+  }
+  Workspace ws(h->scratch, stream);
+  hipError_t e = ws.reserve(bytes);
+  if (e != hipSuccess) return hip_fail(e, "scratch buffer");
+  for (int i = 0; i < t.n; ++i) {
+    void* p = nullptr;
+    e = ws.get(sizeof(float) * (size_t)t.p[i].n_wires * (size_t)binned.p[i].n_ticks, &p);
+    if (e != hipSuccess) return hip_fail(e, "workspace (binned planes)");
+    binned.p[i].image = static_cast<const float*>(p);
+  }
+  {
+    KernelTimer kt("bin_ticks", stream);
+    e = launch_bin_ticks(t, binned, ticks_per_column, stream);
+  }
+  if (e != hipSuccess) return hip_fail(e, "tick binning launch");
+  return classify_hits(h, binned, hits, 3, n_hits, scores, stream, ticks_per_column);
+}
+
 int pointid_classify_requests(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
                               const pointid_request* requests, int32_t n_requests,
                               void* stream_) {
@@ -674,6 +714,21 @@ int pointid_gather_planes(const pointid_plane* planes, int32_t n_planes, const i
   return e == hipSuccess ? POINTID_OK : hip_fail(e, "gather launch");
 }
 
+
+int pointid_downsample(const float* image, int32_t n_wires, int32_t n_ticks,
+                       int32_t ticks_per_column, float* out, void* stream) {
+  if (n_wires <= 0 || n_ticks <= 0) return fail(POINTID_EINVAL, "n_wires and n_ticks must be positive");
+  if (ticks_per_column < 1) return fail(POINTID_EINVAL, "ticks_per_column must be >= 1");
+  if (!image || !out) return fail(POINTID_EINVAL, "NULL device pointer");
+  PlaneTable in, o;
+  std::memset(&in, 0, sizeof(in));
+  std::memset(&o, 0, sizeof(o));
+  in.n = o.n = 1;
+  in.p[0] = {image, n_wires, n_ticks};
+  o.p[0] = {out, n_wires, (int32_t)(((int64_t)n_ticks + ticks_per_column - 1) / ticks_per_column)};
+  hipError_t e = launch_bin_ticks(in, o, ticks_per_column, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? POINTID_OK : hip_fail(e, "tick binning launch");
+}
 
 int pointid_find_hits(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
                       float threshold, int32_t* hits_out, int64_t capacity, int64_t* n_found,

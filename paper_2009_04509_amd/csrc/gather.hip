@@ -23,10 +23,13 @@ namespace {
 
 constexpr int kWaves = 4;                 // patches per block (one per wave)
 
-// Hit i of a hit array: (wire, tick) on plane 0 (stride 2) or (plane, wire, tick).
+// Hit i of a hit array: (wire, tick) on plane 0 (stride 2) or (plane, wire,
+// tick); with `div` ticks per image column the tick becomes its column,
+// floor(tick / div).
 struct HitArray {
   const int32_t* hits;
   int stride;
+  int div;
   __device__ void get(int64_t i, int& plane, int& w, int& t) const {
     const int32_t* h = hits + i * stride;
     if (stride == 3) {
@@ -37,6 +40,10 @@ struct HitArray {
       plane = 0;
       w = h[0];
       t = h[1];
+    }
+    if (div > 1) {
+      const int q = t / div;
+      t = (q * div != t && t < 0) ? q - 1 : q;
     }
   }
 };
@@ -181,7 +188,44 @@ __global__ __launch_bounds__(256) void to_16_kernel(const float4* __restrict__ i
                       Op::pack(b.z, b.w));
 }
 
+// Columns of D ticks (paper §2.1: a pixel holds the charge its wire collects in
+// the time interval of its column): out[w][j] is the charge per tick of the
+// interval, the sum of in[w][jD + k] over the ticks k < D that exist divided by
+// D (missing ticks count as 0), accumulated in fp64 in tick order and rounded
+// to fp32 once.  blockIdx.z is the plane, blockIdx.y strides over wires, and the
+// lanes of a block take consecutive columns, so a wave's loads of one k cover
+// consecutive memory.
+__global__ __launch_bounds__(256) void bin_ticks_kernel(PlaneTable in, PlaneTable out, int D) {
+  const int p = blockIdx.z;
+  const int64_t T = in.p[p].n_ticks;
+  const int64_t J = out.p[p].n_ticks;
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= J) return;
+  const int n = (int)(T - j * D < D ? T - j * D : D);
+  float* o = const_cast<float*>(out.p[p].image);
+  for (int64_t w = blockIdx.y; w < in.p[p].n_wires; w += gridDim.y) {
+    const float* x = in.p[p].image + w * T + j * D;
+    double s = x[0];
+    for (int k = 1; k < n; ++k) s += x[k];
+    o[w * J + j] = (float)(s / D);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_bin_ticks(const PlaneTable& in, const PlaneTable& out, int ticks_per_column,
+                            hipStream_t stream) {
+  int64_t jmax = 0, wmax = 0;
+  for (int i = 0; i < in.n; ++i) {
+    if (out.p[i].n_ticks > jmax) jmax = out.p[i].n_ticks;
+    if (in.p[i].n_wires > wmax) wmax = in.p[i].n_wires;
+  }
+  if (jmax <= 0 || in.n <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((jmax + 255) / 256), (unsigned)(wmax < 65535 ? wmax : 65535),
+                  (unsigned)in.n);
+  bin_ticks_kernel<<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
+  return hipGetLastError();
+}
 
 hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t* out,
                                 hipStream_t stream) {
@@ -213,8 +257,9 @@ hipError_t launch_gather_src(const PlaneTable& planes, const Src& src, int64_t n
 
 hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
                          int hit_stride, int64_t n, void* out, int out_dtype,
-                         hipStream_t stream) {
-  return launch_gather_src(planes, HitArray{hits, hit_stride}, n, out, out_dtype, stream);
+                         hipStream_t stream, int tick_div) {
+  return launch_gather_src(planes, HitArray{hits, hit_stride, tick_div}, n, out, out_dtype,
+                           stream);
 }
 
 hipError_t launch_gather_requests(const PlaneTable& planes, const RequestTable& reqs, void* out,

@@ -62,10 +62,17 @@ constexpr int64_t kFc1Frags = (int64_t)(kPos / 2) * 3 * 8 * 64;
 
 // Patch construction.  hits: int32 rows of `hit_stride` (2 = (wire, tick) on
 // plane 0, 3 = (plane, wire, tick)).  out: [n][48][48] of `out_dtype`
-// (POINTID_FP32, or POINTID_BF16 / POINTID_FP16 bit patterns, RNE).
+// (POINTID_FP32, or POINTID_BF16 / POINTID_FP16 bit patterns, RNE).  With
+// tick_div > 1 the planes hold columns of tick_div ticks and a hit's tick t
+// selects column floor(t / tick_div).
 hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,
                          int hit_stride, int64_t n, void* out, int out_dtype,
-                         hipStream_t stream);
+                         hipStream_t stream, int tick_div = 1);
+
+// Planes binned into columns of D ticks: out.p[i] is [n_wires][ceil(n_ticks / D)]
+// of in.p[i] (its n_ticks holds that column count).
+hipError_t launch_bin_ticks(const PlaneTable& in, const PlaneTable& out, int ticks_per_column,
+                            hipStream_t stream);
 
 // Several requests classified by one launch sequence (kernel argument, by
 // value): request r owns patches start[r] .. start[r + 1] - 1 of the launch;

@@ -186,3 +186,22 @@ def test_find_hits_validation(b):
     assert "aligned" in b.pointid_last_error()
     assert L.pointid_find_hits(H, good, 1, 1.0, NULL, 5, n_found, NULL) == b.POINTID_EINVAL
     assert "hits_out" in b.pointid_last_error()
+
+
+def test_downsample_validation(b):
+    L = b.lib
+    assert L.pointid_downsample(FAKE, 0, 10, 2, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_downsample(FAKE, 10, 0, 2, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_downsample(FAKE, 10, 10, 0, FAKE, NULL) == b.POINTID_EINVAL
+    assert "ticks_per_column" in b.pointid_last_error()
+    assert L.pointid_downsample(NULL, 10, 10, 2, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_downsample(FAKE, 10, 10, 2, NULL, NULL) == b.POINTID_EINVAL
+    P = b._Plane
+    good = (P * 1)(P(0x1000, 10, 10))
+    assert L.pointid_classify_planes_ds(NULL, good, 1, 2, FAKE, 5, FAKE, NULL) == b.POINTID_EINVAL
+    H = ctypes.c_void_p(0x3000)     # rejected by validation before it is used
+    assert L.pointid_classify_planes_ds(H, good, 1, 0, FAKE, 5, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_planes_ds(H, good, 1, 2, FAKE, -1, FAKE, NULL) == b.POINTID_EINVAL
+    assert L.pointid_classify_planes_ds(H, good, 1, 2, FAKE, 5, ctypes.c_void_p(0x1004), NULL) \
+        == b.POINTID_EINVAL
+    assert L.pointid_classify_planes_ds(H, good, 1, 2, NULL, 0, NULL, NULL) == b.POINTID_OK
