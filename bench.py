@@ -77,6 +77,14 @@ def parse():
                     help="config 5: T host threads, each classifying its share of the requests "
                          "one at a time and waiting for each (directly on its own stream, or "
                          "through the dynamic batcher when --batch-requests K > 0)")
+    ap.add_argument("--server", action="store_true",
+                    help="config 5: requests go through the local request server "
+                         "(pointid_server_*, Unix socket) from --clients T client threads "
+                         "(default 16), host hits in and host scores out; --batch-requests K "
+                         "turns the server's dynamic batcher on")
+    ap.add_argument("--patches", action="store_true",
+                    help="config 5 with --server: clients send pre-cut fp32 patches "
+                         "(9,216 B each, as the paper's clients do) instead of hits")
     ap.add_argument("--batch-delay-us", type=int, default=200,
                     help="config 5 with --clients: the batcher's longest wait for a fuller batch")
     ap.add_argument("--ticks-per-column", type=int, default=1, metavar="D",
@@ -262,8 +270,25 @@ def serving(args, torch, pid, synth):
     order = [(s, k) for k in range(args.per_stream) for s in range(len(reqs))]
 
     T = args.clients
+    if args.server and T <= 0:
+        T = 16
     batcher = pid.Batcher(h, imgs, max_requests=K, max_delay_us=args.batch_delay_us) \
-        if (T > 0 and K > 0) else None
+        if (T > 0 and K > 0 and not args.server) else None
+    server = None
+    if args.server:
+        import tempfile
+        sock_dir = tempfile.mkdtemp(prefix="pointid_")
+        sock_path = os.path.join(sock_dir, "bench.sock")
+        server = pid.Server(h, imgs, sock_path, max_requests=K, max_delay_us=args.batch_delay_us)
+        clients = [pid.Client(sock_path) for _ in range(T)]
+        host_hits = [[x for (_, x) in rs] for rs in reqs]
+        host_patches = None
+        if args.patches:
+            # the clients' pre-cut patches, made once before timing with the
+            # library's own gather and kept in host memory
+            host_patches = [[pid.pointid_gather(imgs[p], hits[s][k]).cpu().numpy()
+                             for k, (p, _) in enumerate(rs)] for s, rs in enumerate(reqs)]
+        server_ns = []
 
     def client_step():
         """T synchronous clients; per-request latency measured on the host."""
@@ -274,7 +299,13 @@ def serving(args, torch, pid, synth):
             st = streams[c % len(streams)]
             for s, k in order[c::T]:
                 t0 = time.perf_counter()
-                if batcher is not None:
+                if server is not None:
+                    if host_patches is not None:
+                        clients[c].classify_patches(host_patches[s][k])
+                    else:
+                        clients[c].classify(host_hits[s][k], plane=reqs[s][k][0])
+                    server_ns.append(clients[c].server_ns)
+                elif batcher is not None:
                     batcher.wait(batcher.submit(reqs[s][k][0], hits[s][k], outs[s][k]))
                 else:
                     pid.pointid_classify(h, imgs[reqs[s][k][0]], hits[s][k], outs[s][k], stream=st)
@@ -353,6 +384,9 @@ def serving(args, torch, pid, synth):
                                f"{lo_hits:,}-{hi_hits:,} hits, " + (
                                    f"{T} client threads, each waiting for its request; " if T > 0
                                    else "") + (
+                                   ("through the local request server (Unix socket, host " +
+                                    ("patches" if args.patches else "hits") + " in, host scores "
+                                    "out), ") if server is not None else "") + (
                                    (f"dynamic batcher (up to {K} requests, {args.batch_delay_us} us)"
                                     if T > 0 else
                                     f"batches of {K} requests per pointid_classify_requests call")
@@ -365,6 +399,13 @@ def serving(args, torch, pid, synth):
                        "mean": round(float(lat.mean()), 4)},
         "kernels": kern,
     }
+    if server is not None:
+        sn = np.asarray(server_ns, np.float64) / 1e6
+        out["server_ms"] = {"p50": round(float(np.percentile(sn, 50)), 4),
+                            "p99": round(float(np.percentile(sn, 99)), 4)}
+        for c in clients:
+            c.close()
+        server.close()
     if batcher is not None:
         batcher.close()
     h.close()

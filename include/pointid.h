@@ -57,7 +57,8 @@ enum {
     POINTID_ENOMEM = -2,        /* device allocation failed */
     POINTID_EHIP = -3,          /* a HIP runtime call or kernel launch failed */
     POINTID_ENODEV = -4,        /* no usable gfx950 device */
-    POINTID_EUNSUPPORTED = -5   /* precision or dtype not supported */
+    POINTID_EUNSUPPORTED = -5,  /* precision or dtype not supported */
+    POINTID_EIO = -6            /* socket I/O failed or the peer closed (server / client) */
 };
 
 /* arithmetic of a handle (pointid_create) or element type of a patch buffer */
@@ -310,6 +311,57 @@ int pointid_downsample(const float *image, int32_t n_wires, int32_t n_ticks,
 int pointid_find_hits(pointid_handle h, const pointid_plane *planes,
                       int32_t n_planes, float threshold, int32_t *hits_out,
                       int64_t capacity, int64_t *n_found, void *stream);
+
+/*
+ * Local request server (paper §2.3: the module's model interface sends its
+ * inputs to an inference server and blocks until the scores return; many
+ * client processes share one GPU and the server merges their requests).
+ * pointid_server_start listens on the Unix-domain stream socket
+ * `socket_path` (created; it must not exist) and serves each connection on a
+ * thread of its own, one request at a time:
+ *   - hits (wire, tick) on one of the resident `planes`, or (plane, wire,
+ *     tick) over all of them: classified through a dynamic batcher
+ *     (pointid_batcher_*, max_requests / max_delay_us) when max_requests > 0,
+ *     else by one pointid_classify(_planes) call per request;
+ *   - pre-cut fp32 patches (the paper's transmitted inputs):
+ *     pointid_classify_patches per request.
+ * Scores are bit for bit those of the direct calls.  The handle and the plane
+ * images must outlive the server.  A request may hold up to 4,194,304 hits or
+ * patches.  Wire format: 32-byte headers, see the library source.
+ *   n_planes  0..64 (0: patches only)
+ * start errors: EINVAL (NULL handle or out; bad plane; negative sizes; path
+ * NULL, empty or longer than 107 bytes), EIO (socket, bind -- e.g. the path
+ * exists -- or listen failed), ENOMEM, EHIP.
+ * pointid_server_stop closes the socket, lets each connection finish the
+ * request it is serving, joins the threads and removes the socket file.
+ */
+typedef struct pointid_server_s *pointid_server;
+int pointid_server_start(pointid_handle h, const pointid_plane *planes,
+                         int32_t n_planes, const char *socket_path,
+                         int32_t max_requests, int32_t max_delay_us,
+                         pointid_server *out);
+int pointid_server_stop(pointid_server s);
+
+/*
+ * Client of a local request server (plain sockets: no GPU, no HIP call).  All
+ * buffers are HOST memory; a call blocks until the scores are back.  One
+ * client handle serves one thread at a time.
+ *   plane >= 0: hits int32 [n_hits][2] = (wire, tick) on that plane;
+ *   plane <  0: hits int32 [n_hits][3] = (plane, wire, tick)
+ *   scores fp32 [n][4]
+ *   server_ns (optional, may be NULL): time the server spent on the request,
+ *   from its header to its scores being ready, in nanoseconds
+ * Errors: EINVAL (NULL client or pointer, n out of [0, 4194304], bad path),
+ * EIO (connect, send or receive failed, malformed response), or the status the
+ * server returned (EINVAL for a plane it does not hold, ENOMEM, EHIP).
+ */
+typedef struct pointid_client_s *pointid_client;
+int pointid_client_connect(const char *socket_path, pointid_client *out);
+int pointid_client_classify(pointid_client c, int32_t plane, const int32_t *hits,
+                            int64_t n_hits, float *scores, int64_t *server_ns);
+int pointid_client_classify_patches(pointid_client c, const float *patches,
+                                    int64_t n, float *scores, int64_t *server_ns);
+int pointid_client_close(pointid_client c);
 
 /*
  * Kernel timing for measurement tools (not needed for classification).  While

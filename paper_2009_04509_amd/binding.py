@@ -24,12 +24,14 @@ POINTID_ENOMEM = -2
 POINTID_EHIP = -3
 POINTID_ENODEV = -4
 POINTID_EUNSUPPORTED = -5
+POINTID_EIO = -6
 POINTID_FP32 = 0
 POINTID_BF16 = 1
 POINTID_FP16 = 2
 MAX_PLANES = 64
 
-_STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ENODEV", -5: "EUNSUPPORTED"}
+_STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ENODEV", -5: "EUNSUPPORTED",
+           -6: "EIO"}
 _WEIGHT_FIELDS = ("conv_w", "conv_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b",
                   "cls_w", "cls_b", "mic_w", "mic_b")
 _WEIGHT_SIZES = {"conv_w": 48 * 25, "conv_b": 48, "fc1_w": 92928 * 128, "fc1_b": 128,
@@ -86,6 +88,13 @@ def _load():
         "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
         "pointid_find_hits": (cint, [vp, ctypes.POINTER(_Plane), i32, ctypes.c_float, vp, i64,
                                      vp, vp]),
+        "pointid_server_start": (cint, [vp, ctypes.POINTER(_Plane), i32, ctypes.c_char_p, i32, i32,
+                                        ctypes.POINTER(vp)]),
+        "pointid_server_stop": (cint, [vp]),
+        "pointid_client_connect": (cint, [ctypes.c_char_p, ctypes.POINTER(vp)]),
+        "pointid_client_classify": (cint, [vp, i32, vp, i64, vp, ctypes.POINTER(i64)]),
+        "pointid_client_classify_patches": (cint, [vp, vp, i64, vp, ctypes.POINTER(i64)]),
+        "pointid_client_close": (cint, [vp]),
         "pointid_timing_enable": (cint, [cint]),
         "pointid_timing_reset": (cint, []),
         "pointid_timing_query": (cint, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -107,7 +116,9 @@ EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_c
             "pointid_batcher_wait",
             "pointid_gather",
             "pointid_gather_planes", "pointid_find_hits", "pointid_classify_planes_ds",
-            "pointid_downsample", "pointid_timing_enable", "pointid_timing_reset",
+            "pointid_downsample", "pointid_server_start", "pointid_server_stop",
+            "pointid_client_connect", "pointid_client_classify", "pointid_client_classify_patches",
+            "pointid_client_close", "pointid_timing_enable", "pointid_timing_reset",
             "pointid_timing_query", "pointid_last_error", "pointid_version")
 
 
@@ -441,3 +452,79 @@ def pointid_find_hits(h: Handle, images, threshold: float, capacity: int | None 
                                  _ptr(hits_out) if cap > 0 else ctypes.c_void_p(0), cap,
                                  _ptr(n_found), _stream_ptr(stream, dev)))
     return hits_out, n_found
+
+
+class Server:
+    """pointid_server_start / pointid_server_stop: a local request server over
+    resident device planes (the handle and the planes must outlive it)."""
+
+    def __init__(self, h: Handle, images, socket_path: str, max_requests: int = 0,
+                 max_delay_us: int = 200):
+        self._images = list(images)
+        arr = _plane_array(self._images) if self._images else None
+        raw = ctypes.c_void_p()
+        _check(lib.pointid_server_start(h.raw, arr, len(self._images), socket_path.encode(),
+                                        int(max_requests), int(max_delay_us), ctypes.byref(raw)))
+        self._raw = raw
+        self._h = h
+        self.path = socket_path
+
+    def close(self):
+        if self._raw:
+            _check(lib.pointid_server_stop(self._raw))
+            self._raw = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Client:
+    """pointid_client_*: host arrays in, host scores out (numpy; no GPU)."""
+
+    def __init__(self, socket_path: str):
+        raw = ctypes.c_void_p()
+        _check(lib.pointid_client_connect(socket_path.encode(), ctypes.byref(raw)))
+        self._raw = raw
+        self.server_ns = 0
+
+    def classify(self, hits: np.ndarray, plane: int = -1) -> np.ndarray:
+        """Scores [n][4] of int32 hits [n][2] on `plane`, or [n][3] when plane < 0."""
+        hits = np.ascontiguousarray(hits, dtype=np.int32)
+        width = 2 if plane >= 0 else 3
+        if hits.ndim != 2 or hits.shape[1] != width:
+            raise ValueError(f"hits must be [n][{width}]")
+        out = np.empty((hits.shape[0], 4), np.float32)
+        ns = ctypes.c_int64()
+        _check(lib.pointid_client_classify(self._raw, int(plane), hits.ctypes.data_as(ctypes.c_void_p),
+                                           hits.shape[0], out.ctypes.data_as(ctypes.c_void_p),
+                                           ctypes.byref(ns)))
+        self.server_ns = ns.value
+        return out
+
+    def classify_patches(self, patches: np.ndarray) -> np.ndarray:
+        patches = np.ascontiguousarray(patches, dtype=np.float32)
+        if patches.ndim != 3 or patches.shape[1:] != (48, 48):
+            raise ValueError("patches must be [n][48][48]")
+        out = np.empty((patches.shape[0], 4), np.float32)
+        ns = ctypes.c_int64()
+        _check(lib.pointid_client_classify_patches(self._raw,
+                                                   patches.ctypes.data_as(ctypes.c_void_p),
+                                                   patches.shape[0],
+                                                   out.ctypes.data_as(ctypes.c_void_p),
+                                                   ctypes.byref(ns)))
+        self.server_ns = ns.value
+        return out
+
+    def close(self):
+        if self._raw:
+            _check(lib.pointid_client_close(self._raw))
+            self._raw = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -22,7 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpointid.so")
 
 SOURCES = ["api.hip", "batcher.hip", "gather.hip", "fp32_mfma.hip", "conv_fc1_16.hip", "hits.hip",
-           "pack.hip", "tail.hip"]
+           "pack.hip", "server.hip", "tail.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -205,3 +205,83 @@ def test_downsample_validation(b):
     assert L.pointid_classify_planes_ds(H, good, 1, 2, FAKE, 5, ctypes.c_void_p(0x1004), NULL) \
         == b.POINTID_EINVAL
     assert L.pointid_classify_planes_ds(H, good, 1, 2, NULL, 0, NULL, NULL) == b.POINTID_OK
+
+
+def test_server_and_client_validation(b, tmp_path):
+    L = b.lib
+    out = ctypes.c_void_p()
+    path = str(tmp_path / "s.sock").encode()
+    assert L.pointid_server_start(NULL, None, 0, path, 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert "handle" in b.pointid_last_error()
+    H = ctypes.c_void_p(0x3000)     # rejected by validation before it is used
+    assert L.pointid_server_start(H, None, 1, path, 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_server_start(H, None, 0, None, 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_server_start(H, None, 0, b"x" * 200, 0, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_server_start(H, None, 0, path, -1, 0, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_server_stop(NULL) == b.POINTID_OK
+    # no server behind the path
+    assert L.pointid_client_connect(str(tmp_path / "none.sock").encode(), ctypes.byref(out)) \
+        == b.POINTID_EIO
+    assert "connect" in b.pointid_last_error()
+    assert L.pointid_client_connect(None, ctypes.byref(out)) == b.POINTID_EINVAL
+    assert L.pointid_client_classify(NULL, 0, FAKE, 1, FAKE, None) == b.POINTID_EINVAL
+    assert L.pointid_client_classify_patches(NULL, FAKE, 1, FAKE, None) == b.POINTID_EINVAL
+    assert L.pointid_client_close(NULL) == b.POINTID_OK
+
+
+def test_client_wire_protocol_against_a_stub_server(b, tmp_path):
+    # a stub speaking the documented wire format on the CPU: the client sends
+    # a 32-byte header and the payload, and reads back scores, a server status
+    # or, on a malformed response, fails with EIO
+    import socket
+    import struct
+    import threading
+
+    path = str(tmp_path / "stub.sock")
+    srv = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    srv.bind(path)
+    srv.listen(1)
+    seen = []
+
+    def stub():
+        conn, _ = srv.accept()
+        with conn:
+            for reply in ("scores", "status", "garbage"):
+                hdr = b""
+                while len(hdr) < 32:
+                    hdr += conn.recv(32 - len(hdr))
+                magic, kind, plane, _, n, rid = struct.unpack("<IIiiqQ", hdr)
+                width = 2 if plane >= 0 else 3
+                body = b""
+                while len(body) < 4 * width * n:
+                    body += conn.recv(4 * width * n - len(body))
+                seen.append((magic, kind, plane, n, np.frombuffer(body, np.int32).copy()))
+                if reply == "scores":
+                    sc = np.arange(4 * n, dtype=np.float32)
+                    conn.sendall(struct.pack("<IiqQq", 0x52444950, 0, n, rid, 1234) + sc.tobytes())
+                elif reply == "status":
+                    conn.sendall(struct.pack("<IiqQq", 0x52444950, -1, n, rid, 0))
+                else:
+                    conn.sendall(struct.pack("<IiqQq", 0xDEADBEEF, 0, n, rid, 0))
+
+    th = threading.Thread(target=stub)
+    th.start()
+    try:
+        c = b.Client(path)
+        hits = np.array([[3, 7], [4, 8], [5, 9]], np.int32)
+        got = c.classify(hits, plane=2)
+        assert np.array_equal(got, np.arange(12, dtype=np.float32).reshape(3, 4))
+        assert c.server_ns == 1234
+        magic, kind, plane, n, body = seen[0]
+        assert (magic, kind, plane, n) == (0x51444950, 1, 2, 3)
+        assert np.array_equal(body.reshape(3, 2), hits)
+        with pytest.raises(b.PointIdError) as e:
+            c.classify(np.array([[0, 1, 2]], np.int32), plane=-1)
+        assert e.value.status == b.POINTID_EINVAL and seen[1][2] == -1
+        with pytest.raises(b.PointIdError) as e:
+            c.classify(hits, plane=0)
+        assert e.value.status == b.POINTID_EIO
+        c.close()
+    finally:
+        th.join(timeout=10)
+        srv.close()
