@@ -337,6 +337,52 @@ def forward_16bit_emulated(patches, weights, kind: str = "bf16") -> np.ndarray:
     return heads(h2, q)
 
 
+def to_e4m3_rne(x) -> np.ndarray:
+    """Round to the OCP 8-bit float e4m3 (4 exponent bits, bias 7, 3 mantissa
+    bits, largest finite 448, subnormal step 2^-9), nearest even, values beyond
+    448 saturating to +-448; returned as float64."""
+    x = np.asarray(x, np.float64)
+    a = np.abs(x)
+    e = np.maximum(np.floor(np.log2(np.maximum(a, 2.0 ** -40))), -6.0)   # -6: subnormal range
+    q = 2.0 ** (e - 3)
+    r = np.minimum(np.round(a / q) * q, 448.0)                          # np.round: half to even
+    return np.copysign(r, x)
+
+
+def mx_e4m3(blocks) -> np.ndarray:
+    """Microscaled e4m3 along the last axis (OCP MX): each block of values
+    shares the power-of-two scale X = 2^(floor(log2 max|v|) - 8) (8 = the
+    largest e4m3 exponent), and v / X is rounded to e4m3.  Returns the
+    dequantized values X * e4m3(v / X)."""
+    b = np.asarray(blocks, np.float64)
+    m = np.abs(b).max(axis=-1, keepdims=True)
+    X = np.where(m > 0, 2.0 ** (np.floor(np.log2(np.where(m > 0, m, 1.0))) - 8), 1.0)
+    return to_e4m3_rne(b / X) * X
+
+
+def forward_mx_fp8_emulated(patches, weights) -> np.ndarray:
+    """The network with FC1 in microscaled e4m3 (the fp8 MFMA operands of
+    gfx950): the conv as on the fp16 path (fp16 patch and filter), its ReLU
+    output and the FC1 weights quantized in blocks of 32 FC1 inputs — 8
+    consecutive map positions x 4 consecutive channels, one block per output
+    neuron for the weights — then float64 accumulation.  A precision study
+    only: no kernel computes this."""
+    q = quantize_16bit_model(weights, "fp16")
+    P = round16(np.asarray(patches, np.float32), "fp16")
+    A = conv_relu(P, q["conv_w"], q["conv_b"])
+    n = A.shape[0]
+    a = flatten_hwc(A).reshape(n, FM * FM // 8, 8, NCH // 4, 4).transpose(0, 1, 3, 2, 4)
+    a = mx_e4m3(a.reshape(n, FM * FM // 8, NCH // 4, 32))
+    a = a.reshape(n, FM * FM // 8, NCH // 4, 8, 4).transpose(0, 1, 3, 2, 4).reshape(n, FC1_IN)
+    W1 = np.asarray(weights["fc1_w"], np.float64).T.reshape(FC1_OUT, FM * FM // 8, 8, NCH // 4, 4)
+    W1 = mx_e4m3(W1.transpose(0, 1, 3, 2, 4).reshape(FC1_OUT, FM * FM // 8, NCH // 4, 32))
+    W1 = W1.reshape(FC1_OUT, FM * FM // 8, NCH // 4, 8, 4).transpose(0, 1, 3, 2, 4)
+    W1 = W1.reshape(FC1_OUT, FC1_IN).T
+    h1 = dense_relu(a, W1, weights["fc1_b"])
+    h2 = dense_relu(h1, weights["fc2_w"], weights["fc2_b"])
+    return heads(h2, weights)
+
+
 def forward_bf16_emulated(patches, weights) -> np.ndarray:
     """``forward_16bit_emulated`` with bfloat16 operands."""
     return forward_16bit_emulated(patches, weights, "bf16")
