@@ -327,7 +327,9 @@ int pointid_find_hits(pointid_handle h, const pointid_plane *planes,
  *     pointid_classify_patches per request.
  * Scores are bit for bit those of the direct calls.  The handle and the plane
  * images must outlive the server.  A request may hold up to 4,194,304 hits or
- * patches.  Wire format: 32-byte headers, see the library source.
+ * 65,536 patches; a larger one is refused (EINVAL) and its connection
+ * closed.  Wire format: 32-byte request and response headers, then the
+ * payload (documented in the library source).
  *   n_planes  0..64 (0: patches only)
  * start errors: EINVAL (NULL handle or out; bad plane; negative sizes; path
  * NULL, empty or longer than 107 bytes), EIO (socket, bind -- e.g. the path
@@ -351,7 +353,8 @@ int pointid_server_stop(pointid_server s);
  *   scores fp32 [n][4]
  *   server_ns (optional, may be NULL): time the server spent on the request,
  *   from its header to its scores being ready, in nanoseconds
- * Errors: EINVAL (NULL client or pointer, n out of [0, 4194304], bad path),
+ * Errors: EINVAL (NULL client or pointer, n_hits out of [0, 4194304] or n
+ * patches out of [0, 65536], bad path),
  * EIO (connect, send or receive failed, malformed response), or the status the
  * server returned (EINVAL for a plane it does not hold, ENOMEM, EHIP).
  */

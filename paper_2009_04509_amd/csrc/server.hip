@@ -40,7 +40,10 @@ namespace {
 constexpr uint32_t kReqMagic = 0x51444950u;    // "PIDQ"
 constexpr uint32_t kRespMagic = 0x52444950u;   // "PIDR"
 constexpr uint32_t kKindHits = 1, kKindPatches = 2;
-constexpr int64_t kMaxRequest = int64_t(1) << 22;   // hits or patches per request
+// Per-request limits, which bound the buffers a client can make the server
+// allocate: 4,194,304 hits (48 MiB) or 65,536 patches (576 MiB).
+constexpr int64_t kMaxRequest = int64_t(1) << 22;
+constexpr int64_t kMaxPatches = int64_t(1) << 16;
 constexpr size_t kPatchBytes = sizeof(float) * 48 * 48;
 
 struct ReqHeader {
@@ -231,7 +234,7 @@ void pointid_server_s::serve(int fd) {
     std::string err;
     bool keep = true;
     if (q.magic != kReqMagic || (q.kind != kKindHits && q.kind != kKindPatches) || q.n < 0 ||
-        q.n > kMaxRequest) {
+        q.n > (q.kind == kKindPatches ? kMaxPatches : kMaxRequest)) {
       r.status = POINTID_EINVAL;        // the payload length is unknown: drop the connection
       keep = false;
     } else if (q.kind == kKindHits && (q.plane >= (int32_t)planes.size() || planes.empty())) {
@@ -417,7 +420,7 @@ int pointid_client_classify_patches(pointid_client c, const float* patches, int6
                                     float* scores, int64_t* server_ns) {
   using pointid::set_error;
   if (!c) return set_error(POINTID_EINVAL, "client is NULL");
-  if (n < 0 || n > kMaxRequest) return set_error(POINTID_EINVAL, "n must be in [0, 4194304]");
+  if (n < 0 || n > kMaxPatches) return set_error(POINTID_EINVAL, "n must be in [0, 65536]");
   if (n > 0 && (!patches || !scores)) return set_error(POINTID_EINVAL, "NULL pointer");
   return client_call(c, kKindPatches, -1, patches, kPatchBytes * (size_t)n, n, scores, server_ns);
 }

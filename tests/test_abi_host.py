@@ -285,3 +285,13 @@ def test_client_wire_protocol_against_a_stub_server(b, tmp_path):
     finally:
         th.join(timeout=10)
         srv.close()
+
+
+def test_client_request_limits(b):
+    L = b.lib
+    C = ctypes.c_void_p(0x3000)     # rejected by validation before it is used
+    assert L.pointid_client_classify(C, 0, FAKE, (1 << 22) + 1, FAKE, None) == b.POINTID_EINVAL
+    assert L.pointid_client_classify(C, 0, FAKE, -1, FAKE, None) == b.POINTID_EINVAL
+    assert L.pointid_client_classify_patches(C, FAKE, (1 << 16) + 1, FAKE, None) == b.POINTID_EINVAL
+    assert "65536" in b.pointid_last_error()
+    assert L.pointid_client_classify(C, 0, NULL, 5, FAKE, None) == b.POINTID_EINVAL
