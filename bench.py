@@ -87,6 +87,9 @@ def parse():
                          "(9,216 B each, as the paper's clients do) instead of hits")
     ap.add_argument("--batch-delay-us", type=int, default=200,
                     help="config 5 with --clients: the batcher's longest wait for a fuller batch")
+    ap.add_argument("--sort-hits", action="store_true",
+                    help="config 3: hits in (plane, wire, tick) order, as a hit finder emits "
+                         "them, instead of the generator's shuffled order")
     ap.add_argument("--ticks-per-column", type=int, default=1, metavar="D",
                     help="config 3: patches whose columns span D ticks "
                          "(pointid_classify_planes_ds; 1 = pointid_classify_planes)")
@@ -130,6 +133,8 @@ def make_workload(args, torch, pid):
     dev = "cuda:0"
     if args.config == 3:
         planes, h3 = synth.config3()
+        if args.sort_hits:
+            h3 = np.ascontiguousarray(h3[np.lexsort((h3[:, 2], h3[:, 1], h3[:, 0]))])
         imgs = [torch.from_numpy(p.image).to(dev) for p in planes]
         hits = torch.from_numpy(h3).to(dev)
         n = len(h3)
@@ -155,7 +160,8 @@ def make_workload(args, torch, pid):
                 pid.pointid_classify_planes(h, imgs, hits, scores)
 
             desc = {"workload": "event: 18 planes (6x(800,800,480) wires x 6000 ticks fp32 ADC), "
-                                "50,000 hits, one pointid_classify_planes call",
+                                "50,000 hits" + (" in (plane, wire, tick) order" if args.sort_hits
+                                                 else "") + ", one pointid_classify_planes call",
                     "hits": n, "planes": 18, "ticks": 6000}
         sample = dict(kind="planes", images=[p.image for p in planes], hits=h3, D=D)
         hit_bytes = 12

@@ -74,6 +74,16 @@ struct RequestHits {
   }
 };
 
+// Blocks are dispatched round-robin over the 8 XCDs (block b to XCD b % 8).
+// Logical block order: the blocks one XCD runs take consecutive patches, so
+// hits that arrive in wire order share their windows' image lines in that
+// XCD's L2.  A bijection of [0, nb).
+__device__ __forceinline__ int64_t xcd_major_block(int64_t b, int64_t nb) {
+  const int64_t x = b % 8, s = b / 8;
+  const int64_t q = nb / 8, r = nb % 8;
+  return x * q + (x < r ? x : r) + s;
+}
+
 template <int kOut, class Src>
 __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src, int64_t n,
                                                      void* __restrict__ out) {
@@ -84,7 +94,7 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
   constexpr int kWords = kPix / 4 + 1;                   // aligned words covering a chunk
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int64_t i = (int64_t)blockIdx.x * kWaves + wave;
+  const int64_t i = xcd_major_block(blockIdx.x, gridDim.x) * kWaves + wave;
   if (i >= n) return;                                    // wave-uniform
 
   int plane = 0, w = 0, t = 0;
