@@ -232,6 +232,8 @@ def cpu_baseline(sample, n_sample):
         else:
             oracle.classify_planes(sample["images"], sample["hits"][idx], w)
             what = f"{n_sample} hits sampled (seeded) from the 50,000-hit event, oracle.classify_planes"
+        if "what" in sample:
+            what = f"{n_sample} {sample['what']}, oracle.classify_planes"
     elif sample["kind"] == "plane":
         idx = np.sort(rng.choice(len(sample["hits"]), min(n_sample, len(sample["hits"])), replace=False))
         t0 = time.perf_counter()
@@ -380,6 +382,24 @@ def serving(args, torch, pid, synth):
         if cnt:
             kern[name] = {"ms_per_step": round(tot / args.steps, 4), "launches": cnt,
                           "avg_launch_ms": round(tot / cnt, 4)}
+    # the fused kernel over all launches of the timed steps (every request's
+    # patches pass through it once).  When the batches run on one stream (a
+    # batcher's) the launches are timed one by one; when requests run on many
+    # streams at once their launches overlap, and the step's wall clock is the
+    # time base instead.
+    roof = None
+    if "conv_fc1_16" in kern:
+        one_stream = batcher is not None or (server is not None and K > 0)
+        flop = total * args.steps * 2 * (CONV_MAC + FC1_MAC)
+        base_s = (kern["conv_fc1_16"]["ms_per_step"] * args.steps * 1e-3 if one_stream else wall)
+        ach = flop / base_s / 1e12
+        roof = {"kernel": "conv_fc1_16", "bound": "mfma", "achieved": round(ach, 3),
+                "peak": PEAK["mfma_bf16"], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK["mfma_bf16"], 4), "traffic": None,
+                "time_base": "launch events on the batcher's stream" if one_stream else
+                             "wall clock of the steps (launches on many streams overlap)",
+                "avg_launch_ms": kern["conv_fc1_16"]["avg_launch_ms"],
+                "work_per_launch": flop / kern["conv_fc1_16"]["launches"]}
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
@@ -403,8 +423,22 @@ def serving(args, torch, pid, synth):
         "latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
                        "p99": round(float(np.percentile(lat, 99)), 4),
                        "mean": round(float(lat.mean()), 4)},
+        "roofline": roof,
         "kernels": kern,
     }
+    if not args.no_cpu_baseline:
+        # the oracle on a seeded sample of the requests' hits (each on its plane)
+        rng = np.random.default_rng(2025)
+        flat = [(p, x) for rs in reqs for (p, x) in rs]
+        pick = rng.choice(len(flat), 6, replace=False)
+        imgs_np = [pl.image for pl in planes]
+        parts = []
+        for r in pick:
+            p, x = flat[r]
+            parts.append(np.c_[np.full(len(x), p, np.int32), x])
+        h3s = np.concatenate(parts)[:args.cpu_sample]
+        out["cpu_baseline"] = cpu_baseline(dict(kind="planes", images=imgs_np, hits=h3s,
+                                                what="hits of 6 seeded requests"), len(h3s))
     if server is not None:
         sn = np.asarray(server_ns, np.float64) / 1e6
         out["server_ms"] = {"p50": round(float(np.percentile(sn, 50)), 4),
