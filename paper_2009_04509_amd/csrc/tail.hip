@@ -4,13 +4,15 @@
 //
 // A block of 256 threads handles 32 patches.
 //   1. Each thread owns one float4 column slice of 4 patch rows; it issues the
-//      loads of all the splits' partials at once (coalesced 512 B rows), then
+//      loads of 4 splits' partials at once (coalesced 512 B rows), twice, and
 //      adds them in ascending split order, adds b1, applies ReLU and stores h1
 //      in LDS.
-//   2. A group of 32 lanes evaluates one patch at a time: lane j keeps column j
-//      of W2 in registers (staged once per block through LDS) and forms h2[j]
-//      from h1 broadcast out of LDS; the four head inputs are reduced across
-//      the 32 lanes by a fixed butterfly.
+//   2. A wave evaluates one patch at a time: lane (half, j) keeps rows
+//      64 half .. 64 half + 63 of column j of W2 in registers (staged once per
+//      block through LDS) and forms its half of h2[j] from h1 broadcast out of
+//      LDS; the halves are added across lanes j and j + 32, and the four head
+//      inputs are reduced across 32 lanes by a fixed butterfly.
+// Both phases fit in about 90 registers, so 4 waves share a SIMD.
 // Every patch is computed by the same instruction sequence whatever its
 // position, so results do not depend on the batch or the hit order.
 #include "internal.h"
@@ -19,7 +21,7 @@ namespace pointid {
 namespace {
 
 constexpr int kRows = 32;                   // patches per block
-constexpr int kMaxSplits = 8;               // splits whose loads are in flight together
+constexpr int kMaxSplits = 4;               // splits whose loads are in flight together
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 typedef float vec4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) vec4 global_float4;
@@ -105,27 +107,31 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
   }
   __syncthreads();
 
-  // ---- 2. FC2 + heads, 32 lanes per patch
+  // ---- 2. FC2 + heads, one wave per patch
   const int j = tid & 31;
-  const int grp = tid >> 5;                  // 8 groups
-  float wc[kFc1Out];
+  const int half = (tid >> 5) & 1;
+  const int wave = tid >> 6;                 // 4 waves
+  constexpr int kHalfIn = kFc1Out / 2;
+  float wc[kHalfIn];
 #pragma unroll
-  for (int i = 0; i < kFc1Out; ++i) wc[i] = W2s[i * kFc2Out + j];
+  for (int i = 0; i < kHalfIn; ++i) wc[i] = W2s[(half * kHalfIn + i) * kFc2Out + j];
   const float b2 = w.fc2_b[j];
   const float c0 = w.cls_w[j * 3 + 0], c1 = w.cls_w[j * 3 + 1], c2 = w.cls_w[j * 3 + 2];
   const float mw = w.mic_w[j];
   const float cb0 = w.cls_b[0], cb1 = w.cls_b[1], cb2 = w.cls_b[2], mb = w.mic_b[0];
-  for (int r = grp; r < kRows; r += 8) {
+  for (int r = wave; r < kRows; r += 4) {
     if (p0 + r >= n) break;
-    float h = 0.f;
+    float hp = 0.f;
 #pragma unroll
-    for (int i = 0; i < kFc1Out; ++i) h = fmaf(H[r][i], wc[i], h);
-    h = fmaxf(h + b2, 0.f);
+    for (int i = 0; i < kHalfIn; ++i) hp = fmaf(H[r][half * kHalfIn + i], wc[i], hp);
+    // both halves form (inputs 0-63) + (inputs 64-127)
+    const float ho = __shfl_xor(hp, 32);
+    const float h = fmaxf((half == 0 ? hp + ho : ho + hp) + b2, 0.f);
     const float z0 = sum32(h * c0) + cb0;
     const float z1 = sum32(h * c1) + cb1;
     const float z2 = sum32(h * c2) + cb2;
     const float q = sum32(h * mw) + mb;
-    if (j == 0) {
+    if (tid % 64 == 0) {
       const float zm = fmaxf(z0, fmaxf(z1, z2));
       const float e0 = expf(z0 - zm), e1 = expf(z1 - zm), e2 = expf(z2 - zm);
       const float inv = 1.f / (e0 + e1 + e2);
