@@ -100,9 +100,9 @@ __global__ __launch_bounds__(64 * kMaskWaves) void hits_mask_kernel(PlaneTable p
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const bool live = g + u < end;                     // wave-uniform
-      const int T = c.T;
+      const int64_t T = c.T;
       const float* x = c.x;
-      const int t0 = c.s * kHitStep + 4 * lane;
+      const int64_t t0 = (int64_t)c.s * kHitStep + 4 * lane;
       if constexpr (kVec) {
         if (live && t0 < T) {                             // T % 4 == 0: all 4 inside
           const float4 q = *reinterpret_cast<const float4*>(x + t0);
@@ -118,7 +118,7 @@ __global__ __launch_bounds__(64 * kMaskWaves) void hits_mask_kernel(PlaneTable p
         for (int j = 0; j < 4; ++j) v[u][j] = (live && t0 + j < T) ? x[t0 + j] : ninf;
       }
       // lane 0 needs the tick before the step, lane 63 the tick after it
-      const int te = lane == 0 ? c.s * kHitStep - 1 : (c.s + 1) * kHitStep;
+      const int64_t te = lane == 0 ? (int64_t)c.s * kHitStep - 1 : ((int64_t)c.s + 1) * kHitStep;
       edge[u] = (live && (lane == 0 || lane == 63) && te >= 0 && te < T) ? x[te] : ninf;
       if (live) advance(planes, st, c);
     }

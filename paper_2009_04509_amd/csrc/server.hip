@@ -27,6 +27,7 @@
 #include <cerrno>
 #include <chrono>
 #include <cstring>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -142,6 +143,13 @@ struct Buffers {
 
 }  // namespace
 
+// One connection: its socket, its thread, and whether the thread has ended.
+struct Conn {
+  int fd = -1;
+  std::thread th;
+  std::atomic<bool> done{false};
+};
+
 struct pointid_server_s {
   pointid_handle h = nullptr;
   int device = 0;
@@ -152,11 +160,11 @@ struct pointid_server_s {
   int wake[2] = {-1, -1};
   std::thread acceptor;
   std::mutex mu;
-  std::vector<std::pair<int, std::thread>> conns;
+  std::vector<std::unique_ptr<Conn>> conns;
   std::atomic<bool> stopping{false};
 
   void accept_loop();
-  void serve(int fd);
+  void serve(Conn* c);
   int handle_request(int fd, const ReqHeader& q, Buffers& buf, hipStream_t s, std::string* err);
 };
 
@@ -221,7 +229,8 @@ int pointid_server_s::handle_request(int fd, const ReqHeader& q, Buffers& buf, h
   return POINTID_OK;
 }
 
-void pointid_server_s::serve(int fd) {
+void pointid_server_s::serve(Conn* conn) {
+  const int fd = conn->fd;
   (void)hipSetDevice(device);
   hipStream_t s = nullptr;
   const bool stream_ok = hipStreamCreate(&s) == hipSuccess;
@@ -256,6 +265,7 @@ void pointid_server_s::serve(int fd) {
   buf.release();
   if (s) (void)hipStreamDestroy(s);
   shutdown(fd, SHUT_RDWR);
+  conn->done.store(true);
 }
 
 void pointid_server_s::accept_loop() {
@@ -272,7 +282,22 @@ void pointid_server_s::accept_loop() {
       close(fd);
       break;
     }
-    conns.emplace_back(fd, std::thread(&pointid_server_s::serve, this, fd));
+    // connections whose clients have gone: join their threads, close their sockets
+    for (size_t i = 0; i < conns.size();) {
+      if (conns[i]->done.load()) {
+        conns[i]->th.join();
+        close(conns[i]->fd);
+        conns[i] = std::move(conns.back());
+        conns.pop_back();
+      } else {
+        ++i;
+      }
+    }
+    auto c = std::make_unique<Conn>();
+    c->fd = fd;
+    Conn* raw = c.get();
+    c->th = std::thread(&pointid_server_s::serve, this, raw);
+    conns.push_back(std::move(c));
   }
 }
 
@@ -366,11 +391,11 @@ int pointid_server_stop(pointid_server s) {
   if (s->acceptor.joinable()) s->acceptor.join();
   {
     std::lock_guard<std::mutex> g(s->mu);
-    for (auto& c : s->conns) shutdown(c.first, SHUT_RDWR);   // a blocked read returns
+    for (auto& c : s->conns) shutdown(c->fd, SHUT_RDWR);     // a blocked read returns
   }
   for (auto& c : s->conns) {
-    if (c.second.joinable()) c.second.join();
-    close(c.first);
+    if (c->th.joinable()) c->th.join();
+    close(c->fd);
   }
   if (s->batcher) (void)pointid_batcher_destroy(s->batcher);
   close(s->listen_fd);

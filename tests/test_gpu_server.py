@@ -155,3 +155,23 @@ def test_bad_request_and_stopped_server(pid, setup):
             c2.classify(reqs[0][0][1][:10], plane=0)
         assert e.value.status == pid.POINTID_EIO
         c2.close()
+
+
+def test_finished_connections_are_reaped(pid, setup):
+    # clients that come and go must not leave sockets or threads behind
+    planes, reqs, imgs, h = setup
+    hits = reqs[1][0][1][:50]
+    with tempfile.TemporaryDirectory() as d:
+        path = os.path.join(d, "pid.sock")
+        srv = pid.Server(h, imgs, path, max_requests=4)
+        c = pid.Client(path)
+        want = c.classify(hits, plane=reqs[1][0][0])
+        c.close()
+        n0 = len(os.listdir("/proc/self/fd"))
+        for _ in range(40):
+            c = pid.Client(path)
+            assert np.array_equal(c.classify(hits, plane=reqs[1][0][0]), want)
+            c.close()
+        n1 = len(os.listdir("/proc/self/fd"))
+        srv.close()
+    assert n1 - n0 <= 3, (n0, n1)
