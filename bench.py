@@ -9,6 +9,7 @@ the heads — over one batch of synthetic input already resident in HBM:
   ticks, fp32 ADC) and 50,000 hits, classified by one pointid_classify_planes
   call;
 * config 2: one 480 x 6000 plane and 3,000 hits (pointid_classify);
+* config 1: one 128 x 512 plane and 128 hits (pointid_classify);
 * config 4: a batch of pre-cut patches (pointid_classify_patches, --batch).
 
 Prints one JSON line on stdout.  `roofline` describes the kernel that takes the
@@ -63,7 +64,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
     ap.add_argument("--streams", type=int, default=64, help="config 5: request streams")
@@ -165,8 +166,8 @@ def make_workload(args, torch, pid):
                     "hits": n, "planes": 18, "ticks": 6000}
         sample = dict(kind="planes", images=[p.image for p in planes], hits=h3, D=D)
         hit_bytes = 12
-    elif args.config == 2:
-        p = synth.config2()
+    elif args.config in (1, 2):
+        p = synth.config1() if args.config == 1 else synth.config2()
         img = torch.from_numpy(p.image).to(dev)
         hits = torch.from_numpy(p.hits).to(dev)
         n = len(p.hits)
@@ -177,8 +178,9 @@ def make_workload(args, torch, pid):
         def step(h):
             pid.pointid_classify(h, img, hits, scores)
 
-        desc = {"workload": "plane: 480 wires x 6000 ticks fp32 ADC, 3,000 hits, one "
-                            "pointid_classify call", "hits": n, "planes": 1, "ticks": 6000}
+        W, T = p.image.shape
+        desc = {"workload": f"plane: {W} wires x {T} ticks fp32 ADC, {n:,} hits, one "
+                            "pointid_classify call", "hits": n, "planes": 1, "ticks": T}
         sample = dict(kind="plane", image=p.image, hits=p.hits)
         hit_bytes = 8
     else:
