@@ -5,8 +5,10 @@
 // (4 fp32 or 8 bf16/fp16 pixels of one patch row), so a wavefront writes 1 KiB
 // of contiguous output per store.  A chunk's pixels are read as the aligned
 // 16-byte words that cover them (the run starts 0-3 floats into the first
-// word) and shifted into place in registers: no LDS, no barrier, and all of a
-// lane's loads are in flight together.  The loads go through a buffer resource
+// word) and shifted into place in registers: no LDS, no barrier.  A lane
+// issues the loads of all its chunks before it shifts any (78 VGPRs, 6 waves
+// per SIMD): with the loads of only two chunks in flight, as the compiler
+// schedules them at 8 waves per SIMD, waves spent most of their time waiting.  The loads go through a buffer resource
 // that starts at the image's 16-byte-aligned base and ends with the image, so
 // a word outside it reads as 0; words partly outside a row hold pixels of the
 // neighbouring row (or bytes just outside the image, in the same 16-byte
@@ -128,6 +130,9 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
   if (small) {
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void*>(base), (short)0, (int)span, 0x00020000);
+    // every load of the wave first (all in flight together), then the shifts
+    floatx4 q[kIter][kWords];
+    int mm[kIter];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
       const int k = lane + 64 * it;
@@ -138,14 +143,23 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
       // byte offset of the chunk's first pixel from `base`; the words are read
       // from the 16-byte boundary below it, `m` floats earlier
       const int64_t rel = (int64_t)lead + 4 * (wire * T + tick0);
-      const int m = (int)((rel >> 2) & 3);
+      mm[it] = (int)((rel >> 2) & 3);
       // offsets are taken mod 2^32: every offset at or past 2^31 is out of range
-      const uint32_t a0 = row_ok ? (uint32_t)(rel - 4 * m) : 0x80000000u;
-      floatx4 q[kWords];
+      const uint32_t a0 = row_ok ? (uint32_t)(rel - 4 * mm[it]) : 0x80000000u;
 #pragma unroll
       for (int j = 0; j < kWords; ++j)
-        q[j] = __builtin_bit_cast(floatx4,
-                                  __builtin_amdgcn_raw_buffer_load_b128(rsrc, a0 + 16u * j, 0, 0));
+        q[it][j] = __builtin_bit_cast(
+            floatx4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, a0 + 16u * j, 0, 0));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int it = 0; it < kIter; ++it) {
+      const int k = lane + 64 * it;
+      const int r = k / kPerRow, hc = k - (k / kPerRow) * kPerRow;
+      const int64_t wire = (int64_t)w - kHalf + r;
+      const int64_t tick0 = (int64_t)t - kHalf + kPix * hc;
+      const bool row_ok = k < kChunks && wire >= 0 && wire < W;
+      const int m = mm[it];
       // pixel j of the chunk is word float m + j: two levels of dword selects
       // (v_perm_b32 byte selects, which the compiler keeps as value operations)
       const uint32_t sel1 = (m & 1) ? 0x07060504u : 0x03020100u;
@@ -153,8 +167,8 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
       uint32_t s1[kPix + 2];
 #pragma unroll
       for (int j = 0; j < kPix + 2; ++j)
-        s1[j] = __builtin_amdgcn_perm(__float_as_uint(q[(j + 1) / 4][(j + 1) % 4]),
-                                      __float_as_uint(q[j / 4][j % 4]), sel1);
+        s1[j] = __builtin_amdgcn_perm(__float_as_uint(q[it][(j + 1) / 4][(j + 1) % 4]),
+                                      __float_as_uint(q[it][j / 4][j % 4]), sel1);
       // columns j_lo <= j < j_hi of the chunk are inside the row
       const int64_t lo64 = -tick0, hi64 = T - tick0;
       const int j_lo = row_ok ? (int)(lo64 < 0 ? 0 : (lo64 > kPix ? kPix : lo64)) : kPix;
