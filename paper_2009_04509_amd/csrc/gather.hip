@@ -219,6 +219,9 @@ __global__ __launch_bounds__(256) void to_16_kernel(const float4* __restrict__ i
 // to fp32 once.  blockIdx.z is the plane, blockIdx.y strides over wires, and the
 // lanes of a block take consecutive columns, so a wave's loads of one k cover
 // consecutive memory.
+// kVec4: D is a multiple of 4 and every row starts 16-byte aligned, so a
+// column is D / 4 whole 16-byte words and lanes read them as such.
+template <bool kVec4>
 __global__ __launch_bounds__(256) void bin_ticks_kernel(PlaneTable in, PlaneTable out, int D) {
   const int p = blockIdx.z;
   const int64_t T = in.p[p].n_ticks;
@@ -229,8 +232,25 @@ __global__ __launch_bounds__(256) void bin_ticks_kernel(PlaneTable in, PlaneTabl
   float* o = const_cast<float*>(out.p[p].image);
   for (int64_t w = blockIdx.y; w < in.p[p].n_wires; w += gridDim.y) {
     const float* x = in.p[p].image + w * T + j * D;
-    double s = x[0];
-    for (int k = 1; k < n; ++k) s += x[k];
+    // the loads of 8 ticks at a time are in flight together; the sum still
+    // runs in tick order from the first tick
+    double s = 0.0;
+    for (int k0 = 0; k0 < n; k0 += 8) {
+      float xs[8];
+      if constexpr (kVec4) {              // n is a multiple of 4 here (T % 4 == 0)
+        const float4* x4 = reinterpret_cast<const float4*>(x + k0);
+        const float4 a = x4[0];
+        const float4 b = k0 + 4 < n ? x4[1] : make_float4(0.f, 0.f, 0.f, 0.f);
+        xs[0] = a.x; xs[1] = a.y; xs[2] = a.z; xs[3] = a.w;
+        xs[4] = b.x; xs[5] = b.y; xs[6] = b.z; xs[7] = b.w;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) xs[k] = k0 + k < n ? x[k0 + k] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (k0 + k < n) s = (k0 + k == 0) ? (double)xs[k] : s + xs[k];
+    }
     o[w * J + j] = (float)(s / D);
   }
 }
@@ -247,7 +267,13 @@ hipError_t launch_bin_ticks(const PlaneTable& in, const PlaneTable& out, int tic
   if (jmax <= 0 || in.n <= 0) return hipSuccess;
   const dim3 grid((unsigned)((jmax + 255) / 256), (unsigned)(wmax < 65535 ? wmax : 65535),
                   (unsigned)in.n);
-  bin_ticks_kernel<<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
+  bool vec4 = ticks_per_column % 4 == 0;
+  for (int i = 0; i < in.n; ++i)
+    vec4 = vec4 && (reinterpret_cast<uintptr_t>(in.p[i].image) & 15) == 0 && in.p[i].n_ticks % 4 == 0;
+  if (vec4)
+    bin_ticks_kernel<true><<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
+  else
+    bin_ticks_kernel<false><<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
   return hipGetLastError();
 }
 
