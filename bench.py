@@ -44,9 +44,8 @@ PEAK = {"mfma_bf16": 2500.0, "mfma_fp32": 157.3, "alu_fp32": 157.3, "hbm": 8000.
 KERNELS = {
     "gather": ("bytes", "gather.hip"),
     "patches_to_16": ("bytes_cast", "gather.hip"),
-    "conv_fp32": ("flops_conv", "fp32_mfma.hip"),
-    "fc1_fp32": ("flops_fc1", "fp32_mfma.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
+    "conv_fc1_f32": ("flops_conv_fc1_f32", "conv_fc1_f32.hip"),
     "tail": ("bytes_tail", "tail.hip"),
     "bin_ticks": ("bytes_bin", "gather.hip"),
     "hits_mask": ("bytes_hits_mask", "hits.hip"),
@@ -623,8 +622,8 @@ def main():
             work = args.steps * per_step_patches * (9216 + 4608)
             unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
         else:
-            mac = {"flops_conv": CONV_MAC, "flops_fc1": FC1_MAC,
-                   "flops_conv_fc1": CONV_MAC + FC1_MAC}[model]
+            mac = {"flops_conv": CONV_MAC, "flops_fc1": FC1_MAC, "flops_conv_fc1": CONV_MAC + FC1_MAC,
+                   "flops_conv_fc1_f32": CONV_MAC + FC1_MAC}[model]
             work = args.steps * per_step_patches * 2 * mac
             unit, rate = "TFLOP/s", work / (tot * 1e-3) / 1e12
         kern[name] = {"ms_per_step": tot / args.steps, "launches": cnt,
@@ -637,7 +636,7 @@ def main():
     model = KERNELS[dom][0]
     if model == "flops_conv_fc1":
         bound, peak = "mfma", PEAK["mfma_bf16"]       # fp16 and bf16 MFMA share one peak
-    elif model in ("flops_fc1", "flops_conv"):
+    elif model in ("flops_fc1", "flops_conv", "flops_conv_fc1_f32"):
         bound, peak = "mfma", PEAK["mfma_fp32"]
     elif model.startswith("flops"):
         bound, peak = "alu", PEAK["alu_fp32"]

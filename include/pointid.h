@@ -371,7 +371,7 @@ int pointid_client_close(pointid_client c);
  * enabled (process-wide), every kernel this library launches is bracketed by
  * two HIP events recorded on the stream the kernel runs on.
  * pointid_timing_query waits for the recorded events of the kernel named
- * `kernel` ("gather", "conv_fp32", "fc1_fp32", "tail", ...) and returns the
+ * `kernel` ("gather", "conv_fc1_16", "conv_fc1_f32", "tail", ...) and returns the
  * summed elapsed milliseconds and the number of launches since the last
  * pointid_timing_reset.  Unknown names return 0 launches.
  * Errors: EINVAL (NULL output pointer), EHIP (event failure).

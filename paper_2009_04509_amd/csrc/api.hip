@@ -223,16 +223,13 @@ class Workspace {
 };
 
 // Scratch bytes of one call: 16-bit or fp32 patches (when the call makes
-// them), the FC1 split-K partials and, on the fp32 path, one chunk of maps.
-constexpr int kSplitsFp32 = 8;            // FC1 split-K on the vector fp32 path
-constexpr int64_t kChunkFp32 = 4096;      // patches whose maps are live at once
+// them) and the FC1 split-K partials.
 size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
   const bool half = precision != POINTID_FP32;
   size_t b = 0;
   if (makes_patches) b += pad256((half ? 2 : 4) * (size_t)n * kPatchPix);
-  const int S = half ? conv_fc1_16_splits() : kSplitsFp32;
+  const int S = half ? conv_fc1_16_splits() : conv_fc1_f32_splits();
   b += pad256(sizeof(float) * (size_t)S * n * kFc1Out);
-  if (!half) b += pad256(sizeof(float) * (size_t)(n < kChunkFp32 ? n : kChunkFp32) * kFc1In);
   return b;
 }
 
@@ -240,27 +237,15 @@ size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
 // requests of `reqs` when it is given.
 int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* scores,
                      hipStream_t stream, Workspace& ws, const RequestTable* reqs = nullptr) {
-  const int S = kSplitsFp32;
+  const int S = conv_fc1_f32_splits();
   float* part = nullptr;
-  float* act = nullptr;
-  const int64_t chunk = n < kChunkFp32 ? n : kChunkFp32;
   hipError_t e = ws.get(sizeof(float) * (size_t)S * n * kFc1Out, (void**)&part);
   if (e != hipSuccess) return hip_fail(e, "workspace (FC1 partials)");
-  e = ws.get(sizeof(float) * (size_t)chunk * kFc1In, (void**)&act);
-  if (e != hipSuccess) return hip_fail(e, "workspace (conv maps)");
-  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
-    const int64_t m = (n - c0) < chunk ? (n - c0) : chunk;
-    {
-      KernelTimer kt("conv_fp32", stream);
-      e = launch_conv_f32(patches + c0 * kPatchPix, m, h->w, act, stream);
-    }
-    if (e != hipSuccess) return hip_fail(e, "conv launch");
-    {
-      KernelTimer kt("fc1_fp32", stream);
-      e = launch_fc1_f32(act, m, c0, n, h->w.fc1_wt, S, part, stream);
-    }
-    if (e != hipSuccess) return hip_fail(e, "fc1 launch");
+  {
+    KernelTimer kt("conv_fc1_f32", stream);
+    e = launch_conv_fc1_f32(patches, n, 0, n, h->w.conv_w, h->w.conv_b, h->w.fc1_wt, part, stream);
   }
+  if (e != hipSuccess) return hip_fail(e, "conv_fc1_f32 launch");
   {
     KernelTimer kt("tail", stream);
     e = reqs ? launch_tail_requests(part, S, h->w, *reqs, stream)

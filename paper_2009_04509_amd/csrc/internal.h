@@ -115,15 +115,13 @@ hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);
 
-// fp32 conv + ReLU on fp32 MFMA for patches [m][2304] -> maps [m][92928] (HWC).
-hipError_t launch_conv_f32(const float* patches, int64_t m, const DeviceWeights& w, float* act,
-                           hipStream_t stream);
-
-// fp32 FC1 partial products on fp32 MFMA: part[s][row0 + i][128] = sum over
-// split s of act[i][k] * W1[k][o], for i < m, from the transposed weights
-// w1t[o][k].  `n_total` is the row count of `part`.
-hipError_t launch_fc1_f32(const float* act, int64_t m, int64_t row0, int64_t n_total,
-                          const float* w1t, int splits, float* part, hipStream_t stream);
+// Fused fp32 conv + ReLU + FC1 on fp32 MFMA: patches [n][2304] fp32 ->
+// part[s][row0 + i][128] for s < conv_fc1_f32_splits(), from the conv filters
+// and biases and the transposed FC1 weights w1t[o][k].
+int conv_fc1_f32_splits();
+hipError_t launch_conv_fc1_f32(const float* patches, int64_t n, int64_t row0, int64_t n_total,
+                               const float* conv_w, const float* conv_b, const float* w1t,
+                               float* part, hipStream_t stream);
 
 // w1t[o][k] = w1[k][o] for the FC1 weights.
 hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream);
