@@ -4,15 +4,18 @@
 //
 // A block of 256 threads handles 32 patches.
 //   1. Each thread owns one float4 column slice of 4 patch rows; it issues the
-//      loads of 4 splits' partials at once (coalesced 512 B rows), twice, and
-//      adds them in ascending split order, adds b1, applies ReLU and stores h1
-//      in LDS.
-//   2. A wave evaluates one patch at a time: lane (half, j) keeps rows
-//      64 half .. 64 half + 63 of column j of W2 in registers (staged once per
-//      block through LDS) and forms its half of h2[j] from h1 broadcast out of
-//      LDS; the halves are added across lanes j and j + 32, and the four head
-//      inputs are reduced across 32 lanes by a fixed butterfly.
-// Both phases fit in about 90 registers, so 4 waves share a SIMD.
+//      loads of 4 (or, in a small launch, all 8) splits' partials at once
+//      (coalesced 512 B rows) and adds them in ascending split order, adds b1,
+//      applies ReLU and stores h1 in LDS.
+//   2. W2 (16 KB) is staged once per block through LDS into registers.  In a
+//      launch that fills the chip, a wave evaluates one patch at a time: lane
+//      (half, j) keeps rows 64 half .. 64 half + 63 of column j and forms its
+//      half of h2[j] from h1 broadcast out of LDS, the halves added across
+//      lanes j and j + 32 (116 registers with 4 splits in flight, so 4 waves
+//      share a SIMD).  In a small launch a group of 32 lanes evaluates one
+//      patch at a time, lane j keeping all of column j (fewer patches per lane
+//      in sequence: the lower latency).  The four head inputs are reduced
+//      across 32 lanes by a fixed butterfly.
 // Every patch is computed by the same instruction sequence whatever its
 // position, so results do not depend on the batch or the hit order.
 #include "internal.h"
@@ -21,7 +24,10 @@ namespace pointid {
 namespace {
 
 constexpr int kRows = 32;                   // patches per block
-constexpr int kMaxSplits = 4;               // splits whose loads are in flight together
+// splits whose loads are in flight together: 4 when the launch fills the
+// chip (116 VGPRs, 4 waves per SIMD), all 8 for a small launch, where a second
+// round of loads would only add latency
+constexpr int kFewSplits = 4, kAllSplits = 8;
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 typedef float vec4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) vec4 global_float4;
@@ -56,7 +62,7 @@ struct RequestOut {
   }
 };
 
-template <class Out>
+template <class Out, int kMaxSplits>
 __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
                                                    int64_t n, DeviceWeights w, Out out) {
   __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
@@ -107,31 +113,19 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
   }
   __syncthreads();
 
-  // ---- 2. FC2 + heads, one wave per patch
+  // ---- 2. FC2 + heads
   const int j = tid & 31;
-  const int half = (tid >> 5) & 1;
-  const int wave = tid >> 6;                 // 4 waves
-  constexpr int kHalfIn = kFc1Out / 2;
-  float wc[kHalfIn];
-#pragma unroll
-  for (int i = 0; i < kHalfIn; ++i) wc[i] = W2s[(half * kHalfIn + i) * kFc2Out + j];
   const float b2 = w.fc2_b[j];
   const float c0 = w.cls_w[j * 3 + 0], c1 = w.cls_w[j * 3 + 1], c2 = w.cls_w[j * 3 + 2];
   const float mw = w.mic_w[j];
   const float cb0 = w.cls_b[0], cb1 = w.cls_b[1], cb2 = w.cls_b[2], mb = w.mic_b[0];
-  for (int r = wave; r < kRows; r += 4) {
-    if (p0 + r >= n) break;
-    float hp = 0.f;
-#pragma unroll
-    for (int i = 0; i < kHalfIn; ++i) hp = fmaf(H[r][half * kHalfIn + i], wc[i], hp);
-    // both halves form (inputs 0-63) + (inputs 64-127)
-    const float ho = __shfl_xor(hp, 32);
-    const float h = fmaxf((half == 0 ? hp + ho : ho + hp) + b2, 0.f);
+  auto finish = [&](int r, float h, bool writer) {
+    h = fmaxf(h + b2, 0.f);
     const float z0 = sum32(h * c0) + cb0;
     const float z1 = sum32(h * c1) + cb1;
     const float z2 = sum32(h * c2) + cb2;
     const float q = sum32(h * mw) + mb;
-    if (tid % 64 == 0) {
+    if (writer) {
       const float zm = fmaxf(z0, fmaxf(z1, z2));
       const float e0 = expf(z0 - zm), e1 = expf(z1 - zm), e2 = expf(z2 - zm);
       const float inv = 1.f / (e0 + e1 + e2);
@@ -139,8 +133,46 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
       const float sig = (q >= 0.f) ? 1.f / (1.f + eq) : eq / (1.f + eq);
       *dst[r] = (vec4){e0 * inv, e1 * inv, e2 * inv, sig};
     }
+  };
+  if constexpr (kMaxSplits == kAllSplits) {
+    // small launch: 8 groups of 32 lanes, lane j holding column j of W2
+    const int grp = tid >> 5;
+    float wc[kFc1Out];
+#pragma unroll
+    for (int i = 0; i < kFc1Out; ++i) wc[i] = W2s[i * kFc2Out + j];
+    for (int r = grp; r < kRows; r += 8) {
+      if (p0 + r >= n) break;
+      // the same two half sums, added in the same order, as the full-launch
+      // layout: a patch's bits do not depend on the launch it is in
+      float h0 = 0.f, h1 = 0.f;
+#pragma unroll
+      for (int i = 0; i < kFc1Out / 2; ++i) h0 = fmaf(H[r][i], wc[i], h0);
+#pragma unroll
+      for (int i = kFc1Out / 2; i < kFc1Out; ++i) h1 = fmaf(H[r][i], wc[i], h1);
+      finish(r, h0 + h1, j == 0);
+    }
+  } else {
+    // full launch: a wave per patch, lane (half, j) holding 64 rows of column j
+    const int half = (tid >> 5) & 1;
+    const int wave = tid >> 6;               // 4 waves
+    constexpr int kHalfIn = kFc1Out / 2;
+    float wc[kHalfIn];
+#pragma unroll
+    for (int i = 0; i < kHalfIn; ++i) wc[i] = W2s[(half * kHalfIn + i) * kFc2Out + j];
+    for (int r = wave; r < kRows; r += 4) {
+      if (p0 + r >= n) break;
+      float hp = 0.f;
+#pragma unroll
+      for (int i = 0; i < kHalfIn; ++i) hp = fmaf(H[r][half * kHalfIn + i], wc[i], hp);
+      // both halves form (inputs 0-63) + (inputs 64-127)
+      const float ho = __shfl_xor(hp, 32);
+      finish(r, half == 0 ? hp + ho : ho + hp, tid % 64 == 0);
+    }
   }
 }
+
+// fewer blocks than the chip's CUs: a launch that cannot fill the chip
+constexpr int64_t kSmallLaunch = 256;
 
 }  // namespace
 
@@ -149,7 +181,12 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
   if (n <= 0) return hipSuccess;
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
-  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, PlainOut{scores});
+  if (blocks < kSmallLaunch)
+    tail_kernel<PlainOut, kAllSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
+        part, splits, n, w, PlainOut{scores});
+  else
+    tail_kernel<PlainOut, kFewSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
+        part, splits, n, w, PlainOut{scores});
   return hipGetLastError();
 }
 
@@ -160,7 +197,12 @@ hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeigh
   if (n <= 0) return hipSuccess;
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
-  tail_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(part, splits, n, w, RequestOut{reqs});
+  if (blocks < kSmallLaunch)
+    tail_kernel<RequestOut, kAllSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
+        part, splits, n, w, RequestOut{reqs});
+  else
+    tail_kernel<RequestOut, kFewSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
+        part, splits, n, w, RequestOut{reqs});
   return hipGetLastError();
 }
 
