@@ -222,6 +222,10 @@ class Workspace {
   hipEvent_t done_ = nullptr;
 };
 
+// Pre-cut fp32 batches up to this size are rounded to 16 bits inside the
+// fused kernel (measured crossover: about 4,096 patches).
+constexpr int64_t kInKernelCast = 4096;
+
 // Scratch bytes of one call: 16-bit or fp32 patches (when the call makes
 // them) and the FC1 split-K partials.
 size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
@@ -255,8 +259,9 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
   return POINTID_OK;
 }
 
-// 16-bit handles: patches (bf16 or fp16 [n][2304]) -> scores.
-int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* scores,
+// 16-bit handles: patches (bf16 or fp16 [n][2304], or fp32 when f32_in,
+// rounded by the fused kernel) -> scores.
+int run_network_16(pointid_handle h, const void* patches, bool f32_in, int64_t n, float* scores,
                    hipStream_t stream, Workspace& ws, const RequestTable* reqs = nullptr) {
   const int S = conv_fc1_16_splits();
   float* part = nullptr;
@@ -264,7 +269,7 @@ int run_network_16(pointid_handle h, const uint16_t* patches, int64_t n, float* 
   if (e != hipSuccess) return hip_fail(e, "workspace (FC1 partials)");
   {
     KernelTimer kt("conv_fc1_16", stream);
-    e = launch_conv_fc1_16(h->precision == POINTID_FP16, patches, n, 0, n, h->w.fc1_frag,
+    e = launch_conv_fc1_16(h->precision == POINTID_FP16, patches, f32_in, n, 0, n, h->w.fc1_frag,
                            h->w.conv_frag, part, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "conv_fc1 launch");
@@ -294,8 +299,7 @@ int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hit
     e = launch_gather(planes, hits, stride, n, patches, h->precision, stream, tick_div);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
-  if (half)
-    return run_network_16(h, static_cast<const uint16_t*>(patches), n, scores, stream, ws);
+  if (half) return run_network_16(h, patches, false, n, scores, stream, ws);
   return run_network_fp32(h, static_cast<const float*>(patches), n, scores, stream, ws);
 }
 
@@ -335,8 +339,7 @@ int classify_request_batch(pointid_handle h, const PlaneTable& planes, const Req
     e = launch_gather_requests(planes, reqs, patches, h->precision, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
-  if (half)
-    return run_network_16(h, static_cast<const uint16_t*>(patches), n, nullptr, stream, ws, &reqs);
+  if (half) return run_network_16(h, patches, false, n, nullptr, stream, ws, &reqs);
   return run_network_fp32(h, static_cast<const float*>(patches), n, nullptr, stream, ws, &reqs);
 }
 
@@ -649,10 +652,17 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  // 16-bit handles: up to kInKernelCast patches the fused kernel rounds the
+  // fp32 rows itself (one launch fewer, which is what a small batch pays for);
+  // above, a separate cast writes 16-bit patches, whose rows the fused kernel
+  // then reads at half the bytes
+  const bool half = h->precision != POINTID_FP32;
+  const bool cast = half && n > kInKernelCast;
   Workspace ws(h->scratch, stream);
-  hipError_t e = ws.reserve(scratch_bytes(h->precision, n, h->precision != POINTID_FP32));
+  hipError_t e = ws.reserve(scratch_bytes(h->precision, n, cast));
   if (e != hipSuccess) return hip_fail(e, "scratch buffer");
-  if (h->precision == POINTID_FP32) return run_network_fp32(h, patches, n, scores, stream, ws);
+  if (!half) return run_network_fp32(h, patches, n, scores, stream, ws);
+  if (!cast) return run_network_16(h, patches, true, n, scores, stream, ws);
   uint16_t* pb = nullptr;
   e = ws.get(2 * (size_t)n * kPatchPix, (void**)&pb);
   if (e != hipSuccess) return hip_fail(e, "workspace (16-bit patches)");
@@ -661,7 +671,7 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
     e = launch_patches_to_16(h->precision == POINTID_FP16, patches, n, pb, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "16-bit cast launch");
-  return run_network_16(h, pb, n, scores, stream, ws);
+  return run_network_16(h, pb, false, n, scores, stream, ws);
 }
 
 int pointid_gather(const float* image, int32_t n_wires, int32_t n_ticks,

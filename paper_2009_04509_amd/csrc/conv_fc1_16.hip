@@ -85,9 +85,11 @@ struct Tile {
 static_assert(Tile<kBigTile>::kLdsDwords >= Tile<kSmallTile>::kLdsDwords, "LDS sized by the big tile");
 
 // Patches past the end of the batch are read from the last patch instead:
-// their results are never stored.
-template <int kBt>
-__device__ __forceinline__ uint4 row_chunk_load(const uint16_t* __restrict__ patches, int64_t n,
+// their results are never stored.  `In` is the patches' element type: 16-bit
+// bit patterns (from the gather or the cast), or fp32 pre-cut patches rounded
+// here, on the way into LDS, with the same round-to-nearest-even as the cast.
+template <int kBt, bool kFp16, class In>
+__device__ __forceinline__ uint4 row_chunk_load(const In* __restrict__ patches, int64_t n,
                                                 int64_t p_base, int r, int c) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   const int p = c / 6, h = c - (c / 6) * 6;
@@ -95,8 +97,17 @@ __device__ __forceinline__ uint4 row_chunk_load(const uint16_t* __restrict__ pat
   gp = gp < n ? gp : n - 1;
   // streamed once per block: non-temporal, so it does not push the block's FC1
   // weight slice out of L2
-  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
-                                       patches + gp * kPatchPix + r * kPatch + h * 8)));
+  const In* src = patches + gp * kPatchPix + r * kPatch + h * 8;
+  if constexpr (sizeof(In) == 2) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src)));
+  } else {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src));
+    const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src) + 1);
+    using Op = Op16<kFp16>;
+    return make_uint4(Op::pack(a[0], a[1]), Op::pack(a[2], a[3]), Op::pack(b[0], b[1]),
+                      Op::pack(b[2], b[3]));
+  }
 }
 
 template <int kBt>
@@ -108,12 +119,12 @@ __device__ __forceinline__ void row_chunk_store(uint32_t* lds, int r, int c, con
 }
 
 // `main` and `extra`: wave-uniform, whether this thread has a first / second chunk
-template <int kBt>
-__device__ __forceinline__ void row_load(const uint16_t* __restrict__ patches, int64_t n,
+template <int kBt, bool kFp16, class In>
+__device__ __forceinline__ void row_load(const In* __restrict__ patches, int64_t n,
                                          int64_t p_base, int r, bool main, bool extra,
                                          uint4 (&v)[2]) {
-  if (main) v[0] = row_chunk_load<kBt>(patches, n, p_base, r, threadIdx.x);
-  if (extra) v[1] = row_chunk_load<kBt>(patches, n, p_base, r, threadIdx.x + kThreads);
+  if (main) v[0] = row_chunk_load<kBt, kFp16, In>(patches, n, p_base, r, threadIdx.x);
+  if (extra) v[1] = row_chunk_load<kBt, kFp16, In>(patches, n, p_base, r, threadIdx.x + kThreads);
 }
 
 template <int kBt>
@@ -125,10 +136,10 @@ __device__ __forceinline__ void row_store(uint32_t* lds, int r, bool main, bool 
 
 // One block: patches p_base .. p_base + kBt - 1 (clamped to the batch) and
 // position range `split`.
-template <bool kFp16, int kSplits, int kBt>
+template <bool kFp16, int kSplits, int kBt, class In>
 __device__ __forceinline__ void conv_fc1_block(
     uint32_t* lds, int split, int64_t p_base,
-    const uint16_t* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
+    const In* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
     const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
   using T = Tile<kBt>;
   constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot, kRegion = T::kRegion;
@@ -194,7 +205,8 @@ __device__ __forceinline__ void conv_fc1_block(
     if (tid < 6 * 64) fv = convp[tid];
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
-      if (r0 + j <= loaded_hi) row_load<kBt>(patches, n, p_base, r0 + j, rmain, extra, v[j]);
+      if (r0 + j <= loaded_hi)
+        row_load<kBt, kFp16, In>(patches, n, p_base, r0 + j, rmain, extra, v[j]);
     if (tid < 6 * 64) cwl[tid] = fv;
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
@@ -287,7 +299,7 @@ __device__ __forceinline__ void conv_fc1_block(
     uint4 rv[2];
     const int want_hi = top_row(step + 2);
     const bool new_row = want_hi > loaded_hi;
-    if (new_row) row_load<kBt>(patches, n, p_base, want_hi, rmain, extra, rv);
+    if (new_row) row_load<kBt, kFp16, In>(patches, n, p_base, want_hi, rmain, extra, rv);
 
     const int P = P0 + kKGroups * step + kg;
     uint4 win_next[kOwn];
@@ -427,19 +439,20 @@ __device__ __forceinline__ void conv_fc1_block(
 // Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A
 // patch's sums do not depend on the size of the tile it is in: every MFMA
 // column and every reduction step is per patch.
-template <bool kFp16, int kSplits>
+template <bool kFp16, int kSplits, class In>
 __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
-    const uint16_t* __restrict__ patches, int64_t n, int64_t n_big, const uint4* __restrict__ w1p,
+    const In* __restrict__ patches, int64_t n, int64_t n_big, const uint4* __restrict__ w1p,
     const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[Tile<kBigTile>::kLdsDwords];
   const int split = blockIdx.x % kSplits;
   const int64_t t = blockIdx.x / kSplits;
   if (t < n_big)
-    conv_fc1_block<kFp16, kSplits, kBigTile>(lds, split, t * kBigTile, patches, n, w1p, convp,
-                                             part, row0, n_total);
+    conv_fc1_block<kFp16, kSplits, kBigTile, In>(lds, split, t * kBigTile, patches, n, w1p, convp,
+                                                 part, row0, n_total);
   else
-    conv_fc1_block<kFp16, kSplits, kSmallTile>(lds, split, n_big * kBigTile + (t - n_big) * kSmallTile,
-                                               patches, n, w1p, convp, part, row0, n_total);
+    conv_fc1_block<kFp16, kSplits, kSmallTile, In>(lds, split,
+                                                   n_big * kBigTile + (t - n_big) * kSmallTile,
+                                                   patches, n, w1p, convp, part, row0, n_total);
 }
 
 constexpr int kSplits16 = 8;
@@ -464,10 +477,9 @@ void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
   *n_small = small;
 }
 
-hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int64_t row0,
-                              int64_t n_total, const uint4* w1p, const uint4* convp,
-                              float* part, hipStream_t stream) {
-  if (n <= 0) return hipSuccess;
+template <bool kFp16, class In>
+hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_total,
+                        const uint4* w1p, const uint4* convp, float* part, hipStream_t stream) {
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -475,13 +487,23 @@ hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int
   int64_t n_big = 0, n_small = 0;
   conv_fc1_16_tiles(n, cus, &n_big, &n_small);
   const dim3 grid((unsigned)((n_big + n_small) * kSplits16));
-  if (fp16)
-    conv_fc1_16_kernel<true, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
-        patches, n, n_big, w1p, convp, part, row0, n_total);
-  else
-    conv_fc1_16_kernel<false, kSplits16><<<grid, dim3(kThreads), 0, stream>>>(
-        patches, n, n_big, w1p, convp, part, row0, n_total);
+  conv_fc1_16_kernel<kFp16, kSplits16, In><<<grid, dim3(kThreads), 0, stream>>>(
+      patches, n, n_big, w1p, convp, part, row0, n_total);
   return hipGetLastError();
+}
+
+hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
+                              int64_t n_total, const uint4* w1p, const uint4* convp,
+                              float* part, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if (f32_in) {
+    const float* p = static_cast<const float*>(patches);
+    return fp16 ? launch_typed<true>(p, n, row0, n_total, w1p, convp, part, stream)
+                : launch_typed<false>(p, n, row0, n_total, w1p, convp, part, stream);
+  }
+  const uint16_t* p = static_cast<const uint16_t*>(patches);
+  return fp16 ? launch_typed<true>(p, n, row0, n_total, w1p, convp, part, stream)
+              : launch_typed<false>(p, n, row0, n_total, w1p, convp, part, stream);
 }
 
 }  // namespace pointid

@@ -101,7 +101,8 @@ hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
                           hipStream_t stream);
 
 // Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
-// bits) -> part[s][row0 + i][128] for s < conv_fc1_16_splits().
+// bits, or fp32 when f32_in: rounded in the kernel) -> part[s][row0 + i][128]
+// for s < conv_fc1_16_splits().
 // Error text for pointid_last_error (this thread); returns `code`.
 int set_error(int code, const std::string& msg);
 // Device ordinal of a handle.
@@ -111,7 +112,7 @@ int conv_fc1_16_splits();
 // Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
 // then n_small of 32.
 void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
-hipError_t launch_conv_fc1_16(bool fp16, const uint16_t* patches, int64_t n, int64_t row0,
+hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);
 
