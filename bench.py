@@ -548,8 +548,8 @@ def hit_finding(args, torch, pid, synth):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); "
-              "the per-hit path shards by hits with no exchange, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (got --gpus {args.gpus}); the per-hit "
+              "path would shard by hits or planes, with no exchange between GPUs", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2009_04509_amd import binding as pid
