@@ -170,13 +170,15 @@ class Workspace {
       return wait ? hipStreamWaitEvent(s_, done_, 0) : hipSuccess;
     }
     // a new buffer, sized to the next power of two (at least 4 MiB) so that
-    // requests of varying size share buffers
+    // requests of varying size share buffers; past 1 GiB to the next 256 MiB,
+    // so that a very large call does not reserve up to twice its need
     v.emplace_back();
     const int slot = (int)v.size() - 1;
     v[slot].busy = true;
     g.unlock();
     size_t cap = size_t(4) << 20;
-    while (cap < bytes) cap <<= 1;
+    while (cap < bytes && cap < (size_t(1) << 30)) cap <<= 1;
+    if (cap < bytes) cap = (bytes + (size_t(256) << 20) - 1) & ~((size_t(256) << 20) - 1);
     void* p = nullptr;
     hipEvent_t ev = nullptr;
     hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);

@@ -14,7 +14,9 @@
 #include <condition_variable>
 #include <deque>
 #include <mutex>
+#include <new>
 #include <string>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -159,7 +161,8 @@ int pointid_batcher_create(pointid_handle h, const pointid_plane* planes, int32_
   if (max_requests < 1 || max_requests > 4096)
     return set_error(POINTID_EINVAL, "max_requests must be in [1, 4096]");
   if (max_delay_us < 0) return set_error(POINTID_EINVAL, "max_delay_us is negative");
-  auto* b = new pointid_batcher_s;
+  auto* b = new (std::nothrow) pointid_batcher_s;
+  if (!b) return set_error(POINTID_ENOMEM, "host allocation failed");
   b->h = h;
   b->device = handle_device(h);
   b->planes.assign(planes, planes + n_planes);
@@ -181,8 +184,24 @@ int pointid_batcher_create(pointid_handle h, const pointid_plane* planes, int32_
     delete b;
     return set_error(POINTID_EHIP, std::string("batcher stream/events: ") + hipGetErrorString(e));
   }
-  b->launcher = std::thread([b] { b->launch_loop(); });
-  b->completer = std::thread([b] { b->complete_loop(); });
+  try {
+    b->launcher = std::thread([b] { b->launch_loop(); });
+    b->completer = std::thread([b] { b->complete_loop(); });
+  } catch (const std::system_error& x) {
+    // the launcher ends at once on stop with nothing pending
+    if (b->launcher.joinable()) {
+      {
+        std::lock_guard<std::mutex> lk(b->mu);
+        b->stop = true;
+      }
+      b->cv_work.notify_all();
+      b->launcher.join();
+    }
+    for (hipEvent_t ev : b->free_events) (void)hipEventDestroy(ev);
+    (void)hipStreamDestroy(b->stream);
+    delete b;
+    return set_error(POINTID_ENOMEM, std::string("batcher threads: ") + x.what());
+  }
   *out = b;
   return POINTID_OK;
 }
@@ -216,8 +235,12 @@ int pointid_batcher_submit(pointid_batcher b, const pointid_request* req, uint64
   {
     std::lock_guard<std::mutex> lk(b->mu);
     if (b->stop) return set_error(POINTID_EINVAL, "batcher is being destroyed");
+    try {
+      b->pending.push_back({*req, b->next_ticket, Clock::now()});
+    } catch (const std::bad_alloc&) {
+      return set_error(POINTID_ENOMEM, "host allocation failed");
+    }
     *ticket = b->next_ticket++;
-    b->pending.push_back({*req, *ticket, Clock::now()});
   }
   b->cv_work.notify_one();
   return POINTID_OK;

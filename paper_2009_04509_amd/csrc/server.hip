@@ -29,7 +29,9 @@
 #include <cstring>
 #include <memory>
 #include <mutex>
+#include <new>
 #include <string>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -293,11 +295,18 @@ void pointid_server_s::accept_loop() {
         ++i;
       }
     }
-    auto c = std::make_unique<Conn>();
-    c->fd = fd;
-    Conn* raw = c.get();
-    c->th = std::thread(&pointid_server_s::serve, this, raw);
-    conns.push_back(std::move(c));
+    // a connection the server cannot take (no memory or thread) is closed,
+    // which the client sees as a dropped connection
+    try {
+      auto c = std::make_unique<Conn>();
+      c->fd = fd;
+      Conn* raw = c.get();
+      conns.reserve(conns.size() + 1);
+      c->th = std::thread(&pointid_server_s::serve, this, raw);
+      conns.push_back(std::move(c));
+    } catch (const std::exception&) {
+      close(fd);
+    }
   }
 }
 
@@ -378,7 +387,17 @@ int pointid_server_start(pointid_handle h, const pointid_plane* planes, int32_t 
     delete s;
     return rc;
   }
-  s->acceptor = std::thread(&pointid_server_s::accept_loop, s);
+  try {
+    s->acceptor = std::thread(&pointid_server_s::accept_loop, s);
+  } catch (const std::system_error& x) {
+    close(s->listen_fd);
+    close(s->wake[0]);
+    close(s->wake[1]);
+    unlink(s->path.c_str());
+    if (s->batcher) (void)pointid_batcher_destroy(s->batcher);
+    delete s;
+    return set_error(POINTID_ENOMEM, std::string("server thread: ") + x.what());
+  }
   *out = s;
   return POINTID_OK;
 }
