@@ -3,7 +3,8 @@
 // only in registers, as in the 16-bit kernel (conv_fc1_16.hip), whose layout
 // this kernel follows with fp32 operands.
 //
-// Work split.  A block owns 64 patches (4 MFMA patch tiles) and one of 8
+// Work split.  A block owns 64 patches (4 MFMA patch tiles; 32 in the blocks
+// that finish a small batch, see conv_fc1_f32_tiles) and one of 8
 // contiguous ranges of map positions (split-K, blockIdx % 8, so the blocks on
 // one XCD share a slice of the FC1 weights).  Positions go in pairs (x, x+1),
 // x even; the 5x6 window of a pair (30 pixels), a constant 1.0 for the bias and
@@ -22,11 +23,12 @@
 //          lane (i, g) is W1t[o][that index] for output o = 16m + i: the lane's
 //          16 B at W1t[o][... + 16t + 4g] are its A operands of the 4 chunks, so
 //          the transposed fp32 weights are read as they are (no repacking).
-// 80 MFMAs per wave and K-step (16 conv, 64 FC1) against 4 weight loads, 2
-// filter and 4 swap LDS accesses and a share of the window reads.
+// With 64-patch tiles: 80 MFMAs per wave and K-step (16 conv, 64 FC1) against
+// 4 weight loads, 2 filter and 4 swap LDS accesses and a share of the window
+// reads (half the MFMAs and swap accesses with 32-patch tiles).
 //
-// LDS (dwords): ring of 8 patch rows (64 patches x 52) | conv filter fragments
-// [6 conv tiles][64 lanes][8] | swap buffers [2][8 waves][2 tiles][64 lanes]
+// LDS (dwords): ring of 8 patch rows (patches x 52) | conv filter fragments
+// [6 conv tiles][64 lanes][8] | swap buffers [2][8 waves][own tiles][64 lanes]
 // x 4; the final reduction reuses it from the start.  The four position
 // groups' partial sums are added in a fixed order ((g0 + g2) + (g1 + g3)) and
 // written as fp32 partials [split][patch][128] for the tail kernel: results do
@@ -42,30 +44,43 @@ constexpr int kGroups = 4;                    // position groups
 constexpr int kHalves = 2;                    // output halves
 constexpr int kWaves = kGroups * kHalves;     // 8
 constexpr int kThreads = kWaves * 64;         // 512
-constexpr int kBt = 64;                       // patches per block
-constexpr int kTiles = kBt / 16;              // 4
-constexpr int kOwn = kTiles / kHalves;        // 2: tiles whose conv a wave computes
 constexpr int kMT = 8 / kHalves;              // 4 output tiles per wave
 constexpr int kRing = 8;                      // patch-row ring slots
 constexpr int kRP = 52;                       // LDS row pitch (dwords; 48 used)
-constexpr int kSlot = kBt * kRP;              // dwords per ring slot
 constexpr int kPairsPerRow = kFm / 2;         // 22
 constexpr int kPairs = kPos / 2;              // 968
 constexpr int kPairGroups = kPairs / kGroups; // 242
 constexpr int kPrologueRows = 2 + kK - 1;     // rows of the first two steps
 constexpr int kQ = 6;                         // K-steps per pair (2 shifts x 3 channel tiles)
 constexpr int kSplits = 8;
-constexpr int kFiltOff = kRing * kSlot;
-constexpr int kSwapOff = kFiltOff + kQ * 64 * 8;
-constexpr int kSwapBuf = kWaves * kOwn * 64 * 4;
-constexpr int kMain = kSwapOff + 2 * kSwapBuf;
-constexpr int kRegion = kMT * kTiles * 64 * 4;        // one wave's partial sums
-constexpr int kLds = kMain > 4 * kRegion ? kMain : 4 * kRegion;
-constexpr int kRowChunks = kBt * 12;                  // 16-byte chunks of a patch row
-constexpr int kRowExtra = kRowChunks - kThreads;      // chunks of the first waves' 2nd load
-static_assert(kLds * 4 <= 160 * 1024, "LDS");
-static_assert(kRowExtra > 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads, "whole waves");
+constexpr int kBigTile = 64;                  // patches per block (most blocks)
+constexpr int kSmallTile = 32;                // patches per block (the last ones)
 static_assert(kPairs % kGroups == 0, "whole pair groups");
+
+// Layout of a block of kBt patches (LDS offsets in dwords).  A patch row (192
+// B) of each of the block's patches is kBt x 12 chunks of 16 B: chunk c = tid
+// for the first kRowMain threads, plus c = kThreads + tid for the first
+// kRowExtra threads (whole waves, so no lane diverges).
+template <int kBt>
+struct Tile {
+  static constexpr int kTiles = kBt / 16;                 // 16-patch MFMA tiles
+  static constexpr int kOwn = kTiles / kHalves;           // tiles whose conv a wave computes
+  static constexpr int kSlot = kBt * kRP;                 // dwords per ring slot
+  static constexpr int kFiltOff = kRing * kSlot;
+  static constexpr int kSwapOff = kFiltOff + kQ * 64 * 8;
+  static constexpr int kSwapBuf = kWaves * kOwn * 64 * 4;
+  static constexpr int kMain = kSwapOff + 2 * kSwapBuf;
+  static constexpr int kRegion = kMT * kTiles * 64 * 4;   // one wave's partial sums
+  static constexpr int kLds = kMain > 4 * kRegion ? kMain : 4 * kRegion;
+  static constexpr int kRowChunks = kBt * 12;
+  static constexpr int kRowMain = kRowChunks < kThreads ? kRowChunks : kThreads;
+  static constexpr int kRowExtra = kRowChunks - kRowMain;
+  static_assert(kTiles % kHalves == 0, "whole tiles per output half");
+  static_assert(kLds * 4 <= 160 * 1024, "LDS");
+  static_assert(kRowMain % 64 == 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads,
+                "row chunking in whole waves");
+};
+static_assert(Tile<kBigTile>::kLds >= Tile<kSmallTile>::kLds, "LDS sized by the big tile");
 
 __device__ __forceinline__ floatx4 mfma4(float a, float b, const floatx4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -83,32 +98,36 @@ __device__ __forceinline__ float4 row_chunk(const float* __restrict__ patches, i
   return make_float4(v[0], v[1], v[2], v[3]);
 }
 
+template <int kBt>
 __device__ __forceinline__ void row_store(float* lds, int r, int c, const float4& v) {
   const int p = c / 12, h = c - (c / 12) * 12;
-  *reinterpret_cast<float4*>(lds + (r & (kRing - 1)) * kSlot + p * kRP + 4 * h) = v;
+  *reinterpret_cast<float4*>(lds + (r & (kRing - 1)) * Tile<kBt>::kSlot + p * kRP + 4 * h) = v;
 }
 
-__global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
-    const float* __restrict__ patches, int64_t n, const float* __restrict__ conv_w,
-    const float* __restrict__ conv_b, const float* __restrict__ w1t, float* __restrict__ part,
-    int64_t row0, int64_t n_total) {
-  __shared__ __attribute__((aligned(16))) float lds[kLds];
+// One block: patches p_base .. p_base + kBt - 1 (clamped to the batch) and
+// position range `split`.
+template <int kBt>
+__device__ __forceinline__ void conv_fc1_f32_block(
+    float* lds, int split, int64_t p_base, const float* __restrict__ patches, int64_t n,
+    const float* __restrict__ conv_w, const float* __restrict__ conv_b,
+    const float* __restrict__ w1t, float* __restrict__ part, int64_t row0, int64_t n_total) {
+  using T = Tile<kBt>;
+  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot, kRegion = T::kRegion;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = wave % kGroups;             // position group
   const int nh = wave / kGroups;             // output half; also the half of the tiles it convolves
   const int partner = kg + kGroups * (1 - nh);
-  const bool extra = wave < kRowExtra / 64;  // wave-uniform: a second row chunk
+  const bool rmain = wave < T::kRowMain / 64;   // wave-uniform: a first row chunk
+  const bool extra = wave < T::kRowExtra / 64;  // wave-uniform: a second row chunk
   const int col = lane & 15, grp = lane >> 4;
-  const int split = blockIdx.x % kSplits;
-  const int64_t p_base = (int64_t)(blockIdx.x / kSplits) * kBt;
   const int G0 = (kPairGroups * split) / kSplits;
   const int steps = (kPairGroups * (split + 1)) / kSplits - G0;
   const int P0 = kGroups * G0;
 
   // ---- conv filter fragments: [conv tile q = 3s + t][lane][MFMA i]
-  float* filt = lds + kFiltOff;
+  float* filt = lds + T::kFiltOff;
   for (int e = tid; e < kQ * 64 * 8; e += kThreads) {
     const int i = e & 7, l = (e >> 3) & 63, q = e >> 9;
     const int s = q / 3, t = q - 3 * (q / 3);
@@ -136,14 +155,14 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
       if (r0 + j <= loaded_hi) {
-        v[j][0] = row_chunk(patches, n, p_base, r0 + j, tid);
+        if (rmain) v[j][0] = row_chunk(patches, n, p_base, r0 + j, tid);
         if (extra) v[j][1] = row_chunk(patches, n, p_base, r0 + j, kThreads + tid);
       }
 #pragma unroll
     for (int j = 0; j < kPrologueRows; ++j)
       if (r0 + j <= loaded_hi) {
-        row_store(lds, r0 + j, tid, v[j][0]);
-        if (extra) row_store(lds, r0 + j, kThreads + tid, v[j][1]);
+        if (rmain) row_store<kBt>(lds, r0 + j, tid, v[j][0]);
+        if (extra) row_store<kBt>(lds, r0 + j, kThreads + tid, v[j][1]);
       }
   }
   __syncthreads();
@@ -177,7 +196,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
       out[j] = (floatx4){fmaxf(c[0], 0.f), fmaxf(c[1], 0.f), fmaxf(c[2], 0.f), fmaxf(c[3], 0.f)};
     }
   };
-  floatx4* swp = reinterpret_cast<floatx4*>(lds + kSwapOff);
+  floatx4* swp = reinterpret_cast<floatx4*>(lds + T::kSwapOff);
   auto put = [&](int buf, const floatx4 (&v)[kOwn]) {
 #pragma unroll
     for (int j = 0; j < kOwn; ++j) swp[((buf * kWaves + wave) * kOwn + j) * 64 + lane] = v[j];
@@ -233,7 +252,7 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
     const int want_hi = top_row(step + 2);
     const bool new_row = want_hi > loaded_hi;
     if (new_row) {
-      rv[0] = row_chunk(patches, n, p_base, want_hi, tid);
+      if (rmain) rv[0] = row_chunk(patches, n, p_base, want_hi, tid);
       if (extra) rv[1] = row_chunk(patches, n, p_base, want_hi, kThreads + tid);
     }
 #pragma unroll
@@ -271,8 +290,8 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
       if (q == 2 && new_row) {
         // the slot it overwrites held a row below every row still read; the
         // barrier publishes it before the step that first needs it
-        row_store(lds, want_hi, tid, rv[0]);
-        if (extra) row_store(lds, want_hi, kThreads + tid, rv[1]);
+        if (rmain) row_store<kBt>(lds, want_hi, tid, rv[0]);
+        if (extra) row_store<kBt>(lds, want_hi, kThreads + tid, rv[1]);
         loaded_hi = want_hi;
       }
       __syncthreads();
@@ -320,6 +339,24 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
   }
 }
 
+// Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A
+// patch's sums do not depend on the size of the tile it is in: every MFMA
+// column and every reduction step is per patch.
+__global__ __launch_bounds__(kThreads, 1) void conv_fc1_f32_kernel(
+    const float* __restrict__ patches, int64_t n, int64_t n_big, const float* __restrict__ conv_w,
+    const float* __restrict__ conv_b, const float* __restrict__ w1t, float* __restrict__ part,
+    int64_t row0, int64_t n_total) {
+  __shared__ __attribute__((aligned(16))) float lds[Tile<kBigTile>::kLds];
+  const int split = blockIdx.x % kSplits;
+  const int64_t t = blockIdx.x / kSplits;
+  if (t < n_big)
+    conv_fc1_f32_block<kBigTile>(lds, split, t * kBigTile, patches, n, conv_w, conv_b, w1t, part,
+                                 row0, n_total);
+  else
+    conv_fc1_f32_block<kSmallTile>(lds, split, n_big * kBigTile + (t - n_big) * kSmallTile,
+                                   patches, n, conv_w, conv_b, w1t, part, row0, n_total);
+}
+
 // W1t[o][k] = W1[k][o], once at create: 32 x 32 tiles through LDS, both sides
 // coalesced.
 __global__ __launch_bounds__(256) void transpose_w1_kernel(const float* __restrict__ w1,
@@ -338,6 +375,21 @@ __global__ __launch_bounds__(256) void transpose_w1_kernel(const float* __restri
 
 int conv_fc1_f32_splits() { return kSplits; }
 
+// As for the 16-bit kernel: big tiles fill whole rounds of the CUs (one block
+// per CU), and the rest is cut into small tiles when they fit in one round.
+void conv_fc1_f32_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
+  const int64_t per_round = cus >= kSplits ? cus / kSplits : 1;     // tiles per round
+  int64_t big = n / (kBigTile * per_round) * per_round;
+  const int64_t rest = n - big * kBigTile;
+  int64_t small = (rest + kSmallTile - 1) / kSmallTile;
+  if (small > per_round) {                   // more than one round of small tiles
+    big += (rest + kBigTile - 1) / kBigTile;
+    small = 0;
+  }
+  *n_big = big;
+  *n_small = small;
+}
+
 hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream) {
   static_assert(kFc1In % 32 == 0 && kFc1Out % 32 == 0, "whole 32 x 32 tiles");
   transpose_w1_kernel<<<dim3(kFc1In / 32, kFc1Out / 32), dim3(256), 0, stream>>>(w1, w1t);
@@ -348,10 +400,15 @@ hipError_t launch_conv_fc1_f32(const float* patches, int64_t n, int64_t row0, in
                                const float* conv_w, const float* conv_b, const float* w1t,
                                float* part, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  const int64_t tiles = (n + kBt - 1) / kBt;
-  const dim3 grid((unsigned)(tiles * kSplits));
-  conv_fc1_f32_kernel<<<grid, dim3(kThreads), 0, stream>>>(patches, n, conv_w, conv_b, w1t, part,
-                                                          row0, n_total);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  int64_t n_big = 0, n_small = 0;
+  conv_fc1_f32_tiles(n, cus, &n_big, &n_small);
+  const dim3 grid((unsigned)((n_big + n_small) * kSplits));
+  conv_fc1_f32_kernel<<<grid, dim3(kThreads), 0, stream>>>(patches, n, n_big, conv_w, conv_b, w1t,
+                                                          part, row0, n_total);
   return hipGetLastError();
 }
 

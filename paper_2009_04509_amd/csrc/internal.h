@@ -120,6 +120,8 @@ hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64
 // part[s][row0 + i][128] for s < conv_fc1_f32_splits(), from the conv filters
 // and biases and the transposed FC1 weights w1t[o][k].
 int conv_fc1_f32_splits();
+// Tiles of the fused fp32 launch for n patches on `cus` CUs (64 and 32 patches).
+void conv_fc1_f32_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
 hipError_t launch_conv_fc1_f32(const float* patches, int64_t n, int64_t row0, int64_t n_total,
                                const float* conv_w, const float* conv_b, const float* w1t,
                                float* part, hipStream_t stream);

@@ -276,12 +276,13 @@ def test_permutation_determinism_duplicates(pid, handles, prec):
     assert np.array_equal(one[0].view(np.uint32), base[7].view(np.uint32))
 
 
-@pytest.mark.parametrize("prec", ["bf16", "fp16"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16", "fp16"])
 def test_tile_shapes_give_the_same_bits(pid, handles, prec):
     """A patch's scores do not depend on the batch around it.
 
-    4,196 patches run as 32 tiles of 96 patches plus 4 tiles of 32 (the end of
-    the batch); the same patches classified in other batches land in other
+    4,196 patches run as 32 tiles of 96 patches plus 4 tiles of 32 (16-bit
+    paths), or 64 tiles of 64 plus 4 of 32 (fp32), the small tiles at the end
+    of the batch; the same patches classified in other batches land in other
     tiles and tile shapes, and must give the same bits."""
     h = _handle(handles, prec)
     P = synth.config4_patches(4196, seed=2024)
