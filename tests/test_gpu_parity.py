@@ -198,6 +198,33 @@ def test_gather_planes_config3(pid):
         assert np.array_equal(gotb.view(np.uint16), _bits16(ref, dt))
 
 
+def test_gather_and_classify_64_planes(pid, handles):
+    """The largest plane table (64 planes, the kernel-argument limit), each of
+    its own shape and row pitch, with hits on every plane: the gather is
+    bit-exact and the classification equals that of the pre-cut patches."""
+    rng = np.random.default_rng(64)
+    imgs = []
+    for k in range(64):
+        W, T = int(rng.integers(20, 90)), int(rng.integers(30, 130))
+        imgs.append(synth.coord_image(W, T) * np.float32(1e-3) + np.float32(k))
+    n = 3000
+    pl = rng.integers(0, 64, n)
+    pl[:64] = np.arange(64)                          # every plane, the last one included
+    wires = np.array([rng.integers(-30, imgs[q].shape[0] + 30) for q in pl])
+    ticks = np.array([rng.integers(-30, imgs[q].shape[1] + 30) for q in pl])
+    hh = np.stack([pl, wires, ticks], 1).astype(np.int32)
+    say(f"64 planes, {n} hits")
+    dimgs = [t(x) for x in imgs]
+    got = pid.pointid_gather_planes(dimgs, t(hh), "fp32").cpu().numpy()
+    ref = oracle.gather_patches_planes(imgs, hh)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    for prec in ("fp32", "fp16"):
+        h = _handle(handles, prec)
+        sc = pid.pointid_classify_planes(h, dimgs, t(hh)).cpu().numpy()
+        want = pid.pointid_classify_patches(h, t(ref)).cpu().numpy()
+        assert np.array_equal(sc.view(np.uint32), want.view(np.uint32)), prec
+
+
 # ------------------------------------------------------------------ classify
 
 @pytest.mark.parametrize("prec", PRECS)
