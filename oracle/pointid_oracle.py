@@ -325,9 +325,13 @@ def quantize_16bit_model(weights, kind: str = "bf16") -> dict:
 
 def forward_16bit_emulated(patches, weights, kind: str = "bf16") -> np.ndarray:
     """The network with a 16-bit path's roundings applied — patch, conv filter,
-    conv output (after ReLU) and FC1 filter rounded to ``kind`` — and float64
-    accumulation.  This is what a 16-bit path computes up to its fp32
-    accumulation order; the full-precision ``forward`` remains the reference."""
+    conv output (after ReLU, through float32) and FC1 filter rounded to
+    ``kind`` — and float64 accumulation; the conv bias, FC1 bias, FC2 and the
+    heads stay as given.  This is what a 16-bit path computes up to its fp32
+    accumulation order; the full-precision ``forward`` remains the reference.
+    Pinned by exact closed forms of a single-pixel chain in which each of these
+    roundings, and each rounding the reading leaves out, changes the scores
+    (tests/golden/closed_forms_16bit.json)."""
     q = quantize_16bit_model(weights, kind)
     P = round16(np.asarray(patches, np.float32), kind)
     A = conv_relu(P, q["conv_w"], q["conv_b"])

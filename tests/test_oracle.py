@@ -9,6 +9,7 @@ torch's bfloat16 rounding, and invariances of a per-hit computation.
 import json
 import math
 import os
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -339,6 +340,72 @@ def test_16bit_emulation_rounds_the_right_operands():
         full = oracle.forward(P, w)
         d = np.abs(full - oracle.forward_16bit_emulated(P, w, kind)).max()
         assert 0 < d < 2e-2
+
+
+def _rne(x, bits):
+    """A Fraction rounded to `bits` significant bits, ties to even (normal range)."""
+    if x == 0:
+        return Fraction(0)
+    sign, x = (-1 if x < 0 else 1), abs(x)
+    e = 0
+    while Fraction(2) ** e > x:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= x:
+        e += 1
+    ulp = Fraction(2) ** (e - bits + 1)
+    q = x / ulp
+    n = math.floor(q)
+    r = q - n
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sign * n * ulp
+
+
+def _chain_scores(h):
+    """(softmax of (h, 0, -h), sigmoid of h) written out."""
+    e, f = math.exp(h), math.exp(-h)
+    return np.array([e / (e + 1 + f), 1 / (e + 1 + f), f / (e + 1 + f), 1 / (1 + f)])
+
+
+def test_16bit_emulation_closed_form():
+    """oracle.forward_16bit_emulated against exact closed forms of a
+    single-pixel chain (tests/golden/closed_forms_16bit.json): the chain's steps
+    are checked in exact rational arithmetic, the oracle must reproduce the
+    resulting scores, and every listed mistake — one of the four rounding
+    points dropped, or the FC1 output, the FC2 filter or the conv bias rounded
+    too — moves the scores by far more than the tolerance."""
+    g = _golden("closed_forms_16bit.json")
+    geo = g["geometry"]
+    W, T = geo["plane"]
+    ch, u, v = geo["tap"]
+    for case in g["cases"]:
+        kind, bits = case["kind"], case["bits"]
+        vals = {k: Fraction(x) for k, x in case["inputs"].items()}
+        for name, op, args, value in case["chain"]:
+            a = [vals[x] for x in args.split()]
+            got = {"round": lambda: _rne(a[0], bits), "round32": lambda: _rne(a[0], 24),
+                   "mul": lambda: a[0] * a[1], "add": lambda: a[0] + a[1]}[op]()
+            assert got == Fraction(value), (kind, name)
+            vals[name] = got
+        h2 = Fraction(case["h2"])
+        assert vals["h2"] == h2
+        img = np.zeros((W, T), np.float32)
+        img[tuple(geo["pixel"])] = np.float32(float(vals["a"]))
+        w = _zero_model()
+        w["conv_w"][ch, u, v] = float(vals["kappa"])
+        w["conv_b"][ch] = float(vals["b0"])
+        w["fc1_w"][geo["fc1_row"], geo["fc1_col"]] = float(vals["omega"])
+        w["fc2_w"][geo["fc2"][0], geo["fc2"][1]] = float(vals["beta"])
+        w["cls_w"][geo["fc2"][1]] = [1.0, 0.0, -1.0]
+        w["mic_w"][geo["fc2"][1]] = 1.0
+        for k in ("conv_w", "conv_b", "fc1_w", "fc2_w"):          # the inputs are float32 values
+            assert np.all(w[k].astype(np.float64) == w[k])
+        P = oracle.gather_patches(img, np.array([geo["hit"]]))
+        got = oracle.forward_16bit_emulated(P, w, kind)[0]
+        want = _chain_scores(float(h2))
+        np.testing.assert_allclose(got, want, rtol=0, atol=1e-12, err_msg=kind)
+        for mistake, mh in case["mutants_h2"].items():
+            assert np.abs(_chain_scores(float(Fraction(mh))) - want).max() > 1e-6, (kind, mistake)
 
 
 # ------------------------------------------------------------------ hit finding
