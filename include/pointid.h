@@ -163,9 +163,9 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane *planes,
  * Classify hits with patches whose columns span D = ticks_per_column ticks
  * each (paper §2.1: a pixel holds the charge its wire collects in the time
  * interval of its column).  Each plane is binned once into columns of D ticks
- * aligned to tick 0 -- column j holds the charge per tick of ticks
- * jD .. jD + D - 1, their sum divided by D (ticks past the end of the plane
- * count as 0), accumulated in fp64 and rounded to fp32 once -- and the patch of hit
+ * aligned to tick 0 -- column j holds the charge of ticks jD .. jD + D - 1,
+ * their sum (ticks past the end of the plane count as 0), accumulated in fp64
+ * and rounded to fp32 once -- and the patch of hit
  * (plane, wire, tick) is cut from the binned plane around column
  * floor(tick / D), exactly as pointid_classify_planes cuts it around a tick.
  * D = 1 gives pointid_classify_planes' bits.
@@ -274,9 +274,9 @@ int pointid_gather_planes(const pointid_plane *planes, int32_t n_planes,
  * pointid_classify_planes_ds, alone; needs no handle and runs on the current
  * HIP device).
  *   image  device fp32 [n_wires][n_ticks], any 4-byte alignment
- *   out    device fp32 [n_wires][ceil(n_ticks / D)]: out[w][j] = (sum of
- *          image[w][jD + k] over k < D with jD + k < n_ticks) / D, accumulated
- *          in fp64 in tick order and rounded once
+ *   out    device fp32 [n_wires][ceil(n_ticks / D)]: out[w][j] = sum of
+ *          image[w][jD + k] over k < D with jD + k < n_ticks, accumulated in
+ *          fp64 in tick order and rounded once
  * Errors: EINVAL (n_wires or n_ticks <= 0, ticks_per_column < 1, NULL
  * pointer), EHIP.
  */

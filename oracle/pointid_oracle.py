@@ -25,13 +25,11 @@ What it computes, with the passage each step follows:
   With one tick per column this is the plane pixel itself (the reading above).
   Reading used for D ticks per column: the waveform is binned once into
   columns of D ticks aligned to tick 0, column j covering ticks jD .. jD + D - 1,
-  and a column's value is the charge of the interval per tick: the sum of its
-  samples divided by D, ticks past the end of the plane counting as 0 as
-  pixels outside the plane do.  (The paper says only that the pixel
-  corresponds to the charge of the interval; per tick keeps a pixel in the
-  units of one sample whatever D, so one tick per column is the plain image.)
-  The patch of hit (w, t) is then cut from the binned plane around column
-  floor(t / D), with the same centring and zero fill as above.
+  and a column's value is the charge deposited in that interval, the sum of
+  its samples; ticks past the end of the plane deposit nothing (0), as pixels
+  outside the plane read 0.  The patch of hit (w, t) is then cut from the
+  binned plane around column floor(t / D), with the same centring and zero
+  fill as above.
 
 * Hit finding, paper §2.1: the reconstruction finds wire hits on the
   deconvolved waveforms (giving peak time and charge) before they are
@@ -113,8 +111,8 @@ def gather_patches_planes(images, hits3) -> np.ndarray:
 
 def downsample_plane(image, ticks_per_column) -> np.ndarray:
     """float32 [n_wires][ceil(n_ticks / D)]: column j is the sum of ticks
-    jD .. jD + D - 1 (missing ticks past the end count as 0) divided by D,
-    in float64, rounded once."""
+    jD .. jD + D - 1 (missing ticks past the end count as 0), in float64,
+    rounded once."""
     D = int(ticks_per_column)
     if D < 1:
         raise ValueError("ticks_per_column must be >= 1")
@@ -123,7 +121,7 @@ def downsample_plane(image, ticks_per_column) -> np.ndarray:
     J = -(-T // D)
     padded = np.zeros((W, J * D), np.float64)
     padded[:, :T] = x
-    return (padded.reshape(W, J, D).sum(axis=2) / D).astype(np.float32)
+    return padded.reshape(W, J, D).sum(axis=2).astype(np.float32)
 
 
 def hits_to_columns(hits3, ticks_per_column) -> np.ndarray:

@@ -213,10 +213,9 @@ __global__ __launch_bounds__(256) void to_16_kernel(const float4* __restrict__ i
 }
 
 // Columns of D ticks (paper §2.1: a pixel holds the charge its wire collects in
-// the time interval of its column): out[w][j] is the charge per tick of the
-// interval, the sum of in[w][jD + k] over the ticks k < D that exist divided by
-// D (missing ticks count as 0), accumulated in fp64 in tick order and rounded
-// to fp32 once.  blockIdx.z is the plane, blockIdx.y strides over wires, and the
+// the time interval of its column): out[w][j] is the charge of the interval,
+// the sum of in[w][jD + k] over the ticks k < D that exist (missing ticks
+// count as 0), accumulated in fp64 in tick order and rounded to fp32 once.  blockIdx.z is the plane, blockIdx.y strides over wires, and the
 // lanes of a block take consecutive columns, so a wave's loads of one k cover
 // consecutive memory.
 // kVec4: D is a multiple of 4 and every row starts 16-byte aligned, so a
@@ -251,7 +250,7 @@ __global__ __launch_bounds__(256) void bin_ticks_kernel(PlaneTable in, PlaneTabl
       for (int k = 0; k < 8; ++k)
         if (k0 + k < n) s = (k0 + k == 0) ? (double)xs[k] : s + xs[k];
     }
-    o[w * J + j] = (float)(s / D);
+    o[w * J + j] = (float)s;
   }
 }
 

@@ -1,11 +1,22 @@
 """GPU parity of patches with D ticks per column (pointid_downsample,
 pointid_classify_planes_ds) against the CPU oracle.
 
-Binning averages D fp32 samples; the library sums in fp64 in tick order,
-divides by D and rounds once, the oracle does the same in numpy, so on ADC-like
-data (sums exact in fp64) the binned planes agree value for value.  Scores are held
-to the bars of the plain path: fp32 1e-4, fp16 2e-2 against the oracle, bf16
-2e-3 against the oracle's bf16-rounded network plus the argmax criterion.
+A column holds the charge of its D ticks: the library sums the fp32 samples in
+fp64 in tick order and rounds once, the oracle does the same in numpy, so on
+ADC-like data (sums exact in fp64) the binned planes agree value for value.
+
+Score bars.  The plain path's bars (fp32 1e-4 and fp16 2e-2 against the
+oracle, bf16 2e-3 against the oracle's bf16-rounded network) are stated for
+inputs on the scale of one sample.  A column sums D samples, so the inputs grow
+by up to a factor D; the network is affine between ReLUs, so every
+pre-activation's data part, and with it the rounding error of each fp32 sum
+(and of each 16-bit operand, a relative error), grows by the same factor, and
+so do the logit errors, which bound the score errors.  The bars here are
+therefore the plain path's times D; the near-tie allowance of the argmax
+criterion scales with them.  (Measured on the plane at D = 4 and 6: the fp16
+network's own 16-bit rounding moves the scores by 0.014-0.015, inside even the
+unscaled bar.)  The binning and the column arithmetic are bit-exact and have no
+tolerance at all.
 """
 
 import functools
@@ -76,7 +87,7 @@ def test_downsample_unaligned_base(pid):
         assert np.array_equal(got, oracle.downsample_plane(view.cpu().numpy(), 4)), off
 
 
-def _compare(got, full, emu, prec, what):
+def _compare(got, full, emu, prec, what, D):
     got = np.asarray(got, np.float64)
     ref = emu if prec == "bf16" else full
     err = np.abs(got - ref).max()
@@ -84,9 +95,15 @@ def _compare(got, full, emu, prec, what):
     srt = np.sort(full[:, :3], axis=1)
     gap = srt[:, 2] - srt[:, 1]
     agree = float(np.mean(am_g == am_f))
-    say(f"[{what} {prec}] n={len(got)} max|d|={err:.3g} argmax agree={agree:.5f}")
-    assert err <= TOL[prec], f"{what} {prec}: {err}"
-    tie = 0.2 if prec == "bf16" else 2 * TOL[prec]
+    tol = D * TOL[prec]
+    say(f"[{what} {prec}] n={len(got)} max|d|={err:.3g} (bar {tol:.3g}) argmax agree={agree:.5f}")
+    assert err <= tol, f"{what} {prec}: {err}"
+    # bf16: a flip needs the bf16-rounded network's own gap to be a near tie
+    # (the emulated network is what the path computes, up to fp32 order)
+    if prec == "bf16":
+        srt_e = np.sort(emu[:, :3], axis=1)
+        gap, am_f = srt_e[:, 2] - srt_e[:, 1], emu[:, :3].argmax(1)
+    tie = 2 * tol
     assert not ((am_g != am_f) & (gap >= tie)).any()
     if len(got) >= 1000:
         assert agree >= 0.999
@@ -102,7 +119,7 @@ def test_classify_planes_ds_plane(pid, handles, D):
     for prec, h in handles.items():
         say(f"classify_planes_ds plane D={D} {prec}")
         got = pid.pointid_classify_planes_ds(h, [t(p2.image)], t(h3), D).cpu().numpy()
-        _compare(got, full, emu, prec, f"plane D={D}")
+        _compare(got, full, emu, prec, f"plane D={D}", D)
 
 
 def test_ds_one_tick_is_classify_planes(pid, handles):
@@ -139,7 +156,7 @@ def test_ds_columns_from_floor_division(pid, handles):
     idx = np.random.default_rng(44).choice(n, 512, replace=False)
     P = oracle.gather_patches_planes_ds(imgs_np, h3[idx], D)
     full = oracle.classify_patches(P, weights()).astype(np.float64)
-    _compare(got[idx], full, full, "fp32", "edges D=5")
+    _compare(got[idx], full, full, "fp32", "edges D=5", D)
 
 
 def test_ds_event_sampled(pid, handles):
@@ -154,4 +171,4 @@ def test_ds_event_sampled(pid, handles):
     for prec in ("fp16", "bf16"):
         say(f"classify_planes_ds event D={D} {prec} (50k hits)")
         got = pid.pointid_classify_planes_ds(handles[prec], imgs, t(h3), D).cpu().numpy()
-        _compare(got[idx], full, emu, prec, "event sampled D=4")
+        _compare(got[idx], full, emu, prec, "event sampled D=4", D)
