@@ -4,14 +4,19 @@ Bars:
 * patch gather bit-exact (fp32 copy; bf16 / fp16 round-to-nearest-even);
 * fp32 path: max |d score| <= 1e-4 against the oracle;
 * fp16 path (16-bit MFMA operands): max |d score| <= 2e-2 against the oracle;
-* bf16 path: rounding any one operand to bf16 already moves the oracle's own
-  scores by up to ~0.05 on raw-ADC inputs (measured with the oracle's 16-bit
-  emulation), so it is held to 2e-3 against the oracle's bf16-rounded network
-  (what the path computes, up to fp32 accumulation order) and to the argmax
-  criterion against the full-precision oracle;
-* argmax agreement >= 99.9% where a set has >= 1000 hits, and every
-  disagreement must be a near-tie of the reference (top-2 gap below twice the
-  tolerance).
+* bf16 path: the contract's bar, max |d score| <= 2e-2 against the oracle, is
+  asserted where the bf16 rounding of the operands allows it: on the pre-cut
+  N(0, 1) patches of the patch sweep and on the tiny plane.  On raw-ADC planes
+  rounding the operands to bf16 already moves the oracle's own scores by more
+  than 2e-2 (tests/test_oracle.py measures it), so there the path is held to
+  2e-3 against the oracle's bf16-rounded network (what the path computes, up
+  to fp32 accumulation order) and to the argmax criterion against the
+  full-precision oracle;
+* argmax agreement >= 99.9% where a set has >= 1000 hits.  Every disagreement
+  must be a near tie of the network the path computes: for fp32 and fp16 a
+  top-2 gap of the oracle below twice the tolerance; for bf16 either the
+  bf16-rounded network itself disagrees with the oracle on that hit, or its
+  top-2 gap is below twice the 2e-3 bar.
 Full-size workloads are run in the launch configuration the benchmark times and
 compared on seeded samples of hits that the oracle evaluates one by one.
 """
@@ -106,17 +111,34 @@ def compare(got, ref, tol, what):
     assert err.max() <= tol, f"{what}: max |d score| {err.max()} > {tol}"
 
 
-def check(got, patches, prec, what):
-    """Compare scores of `prec` with the oracle on the same fp32 patches."""
+BF16_BAR = 2e-2          # the contract's bf16 bar against the full-precision oracle
+
+
+def check(got, patches, prec, what, bf16_full_bar=False):
+    """Compare scores of `prec` with the oracle on the same fp32 patches.
+    bf16_full_bar: also assert the contract's 2e-2 bar for bf16 against the
+    full-precision oracle (workloads where bf16 operands allow it)."""
     full = oracle.classify_patches(patches, weights())
     if prec != "bf16":
         compare(got, full, TOL[prec], f"{what} {prec}")
         return
-    emu = oracle.classify_16bit_emulated(patches, weights(), "bf16")
+    emu = np.asarray(oracle.classify_16bit_emulated(patches, weights(), "bf16"), np.float64)
     compare(got, emu, TOL["bf16"], f"{what} bf16 vs bf16-rounded network")
     g = np.asarray(got, np.float64)
-    agree, flips = _argmax_check(g, np.asarray(full, np.float64), 0.2, f"{what} bf16 vs oracle")
-    say(f"[{what} bf16 vs oracle] max|d|={np.abs(g - full).max():.3g} agree={agree:.5f} flips={flips}")
+    f = np.asarray(full, np.float64)
+    err = float(np.abs(g - f).max())
+    am_g, am_f, am_e = g[:, :3].argmax(1), f[:, :3].argmax(1), emu[:, :3].argmax(1)
+    srt = np.sort(emu[:, :3], axis=1)
+    emu_tie = (srt[:, 2] - srt[:, 1]) < 2 * TOL["bf16"]
+    agree = float(np.mean(am_g == am_f)) if len(f) else 1.0
+    say(f"[{what} bf16 vs oracle] max|d|={err:.3g} agree={agree:.5f} flips={int((am_g != am_f).sum())}")
+    # a disagreement with the oracle is one of the bf16-rounded network itself,
+    # or a near tie of that network
+    assert not ((am_g != am_f) & (am_e == am_f) & ~emu_tie).any(), f"{what}: unexplained bf16 argmax flip"
+    if len(f) >= 1000:
+        assert agree >= 0.999, f"{what} bf16: argmax agreement {agree}"
+    if bf16_full_bar:
+        assert err <= BF16_BAR, f"{what} bf16: max |d score| {err} > {BF16_BAR} against the oracle"
 
 
 # ------------------------------------------------------------------ gather
@@ -233,7 +255,7 @@ def test_classify_config1(pid, handles, prec):
     p = cfg(1)
     say(f"classify config1 {prec}")
     got = pid.pointid_classify(h, t(p.image), t(p.hits)).cpu().numpy()
-    check(got, oracle.gather_patches(p.image, p.hits), prec, "config1")
+    check(got, oracle.gather_patches(p.image, p.hits), prec, "config1", bf16_full_bar=True)
 
 
 @pytest.mark.parametrize("prec", PRECS)
@@ -265,7 +287,7 @@ def test_classify_patches_config4(pid, handles, prec, batch):
     got = pid.pointid_classify_patches(h, t(P)).cpu().numpy()
     idx = np.arange(batch) if batch <= 1024 else np.sort(
         np.random.default_rng(batch).choice(batch, 1024, replace=False))
-    check(got[idx], P[idx], prec, f"patches B={batch}")
+    check(got[idx], P[idx], prec, f"patches B={batch}", bf16_full_bar=True)
 
 
 @pytest.mark.parametrize("prec", PRECS)
@@ -277,7 +299,7 @@ def test_classify_patches_large_sampled(pid, handles, prec, batch):
     got = pid.pointid_classify_patches(h, t(P)).cpu().numpy()
     idx = np.sort(np.random.default_rng(batch + 1).choice(batch, 1024, replace=False))
     idx[-1] = batch - 1                                 # the ragged end of the batch
-    check(got[idx], P[idx], prec, f"patches B={batch}")
+    check(got[idx], P[idx], prec, f"patches B={batch}", bf16_full_bar=True)
 
 
 # ------------------------------------------------------------------ invariances and edges
