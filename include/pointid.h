@@ -126,6 +126,21 @@ int pointid_create(const pointid_weights *w, int precision, int device,
 /* Free a handle (synchronises its device first).  NULL is a no-op. */
 int pointid_destroy(pointid_handle h);
 
+/*
+ * Free cached scratch buffers (see "Temporary device memory" above) until the
+ * handle caches at most `keep_bytes`, largest buffers first.  Only idle
+ * buffers are freed: none that a call on another thread is taking, and none
+ * whose last user's work is still running (those stay cached; call again
+ * later).  keep_bytes = 0 frees every idle buffer.  The next call that needs
+ * scratch allocates again.  hipFree may wait for the device.  The cache holds
+ * at most 512 buffers in any case; when they are all taken, a call reuses the
+ * smallest one big enough and waits on its stream for that buffer's last use.
+ *   cached_bytes  (optional, may be NULL) receives the bytes still cached
+ * Errors: EINVAL (NULL handle), EHIP (hipFree failed; the buffers freed before
+ * the failure stay freed).
+ */
+int pointid_trim(pointid_handle h, uint64_t keep_bytes, uint64_t *cached_bytes);
+
 /* Precision the handle was created with, or EINVAL for NULL. */
 int pointid_precision(pointid_handle h);
 
@@ -228,10 +243,17 @@ int pointid_batcher_create(pointid_handle h, const pointid_plane *planes,
 /* Classify every pending request, wait for all, then free.  NULL is a no-op. */
 int pointid_batcher_destroy(pointid_batcher b);
 /* Queue one request (copied; its buffers are not).  *ticket identifies it.
+ * `stream` (a hipStream_t on the handle's device, or NULL for the null
+ * stream) orders the request after the work already enqueued there: submit
+ * records an event on it, and the batch that classifies the request waits for
+ * that event before reading the hits or writing the scores.  So the hits may
+ * still be in production on `stream` (pointid_find_hits, a copy), and the
+ * scores buffer may come from an allocator that orders reuse by `stream`.
  * Errors: EINVAL (NULL argument, bad request as in pointid_classify_requests,
- * batcher being destroyed). */
+ * batcher being destroyed), EHIP (the event could not be recorded on
+ * `stream`). */
 int pointid_batcher_submit(pointid_batcher b, const pointid_request *req,
-                           uint64_t *ticket);
+                           void *stream, uint64_t *ticket);
 /* Block until the request `ticket` is classified: its scores are then in
  * device memory, visible to the host and to every stream.  Returns the status
  * of its batch (EHIP or ENOMEM if that batch failed), or EINVAL for a ticket

@@ -69,6 +69,7 @@ def _load():
     sig = {
         "pointid_create": (cint, [ctypes.POINTER(_Weights), cint, cint, ctypes.POINTER(vp)]),
         "pointid_destroy": (cint, [vp]),
+        "pointid_trim": (cint, [vp, ctypes.c_uint64, ctypes.POINTER(ctypes.c_uint64)]),
         "pointid_precision": (cint, [vp]),
         "pointid_classify": (cint, [vp, vp, i32, i32, vp, i64, vp, vp]),
         "pointid_classify_planes": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp, vp]),
@@ -81,8 +82,8 @@ def _load():
         "pointid_batcher_create": (cint, [vp, ctypes.POINTER(_Plane), i32, i32, i32,
                                           ctypes.POINTER(vp)]),
         "pointid_batcher_destroy": (cint, [vp]),
-        "pointid_batcher_submit": (cint, [vp, ctypes.POINTER(_Request),
-                                          ctypes.POINTER(ctypes.c_uint64)]),
+        "pointid_batcher_submit": (cint, [vp, ctypes.POINTER(_Request), vp,
+                                            ctypes.POINTER(ctypes.c_uint64)]),
         "pointid_batcher_wait": (cint, [vp, ctypes.c_uint64]),
         "pointid_gather": (cint, [vp, i32, i32, vp, i64, vp, cint, vp]),
         "pointid_gather_planes": (cint, [ctypes.POINTER(_Plane), i32, vp, i64, vp, cint, vp]),
@@ -110,7 +111,8 @@ def _load():
 
 
 lib = _load()
-EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_classify",
+EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_trim",
+            "pointid_classify",
             "pointid_classify_planes", "pointid_classify_requests", "pointid_classify_patches",
             "pointid_batcher_create", "pointid_batcher_destroy", "pointid_batcher_submit",
             "pointid_batcher_wait",
@@ -229,6 +231,14 @@ def pointid_create(weights: dict, precision="fp32", device: int = 0) -> Handle:
 
 def pointid_destroy(h: Handle):
     h.close()
+
+
+def pointid_trim(h: Handle, keep_bytes: int = 0) -> int:
+    """Free the handle's idle cached scratch buffers down to keep_bytes;
+    returns the bytes still cached."""
+    cached = ctypes.c_uint64()
+    _check(lib.pointid_trim(h.raw, ctypes.c_uint64(int(keep_bytes)), ctypes.byref(cached)))
+    return int(cached.value)
 
 
 def pointid_classify(h: Handle, image: torch.Tensor, hits: torch.Tensor,
@@ -350,7 +360,12 @@ class Batcher:
         self.raw = raw
         self._live = {}
 
-    def submit(self, plane: int, hits: torch.Tensor, scores: torch.Tensor | None = None) -> int:
+    def submit(self, plane: int, hits: torch.Tensor, scores: torch.Tensor | None = None,
+               stream=None) -> int:
+        """Queue a request; the batch that classifies it starts after the work
+        enqueued on `stream` (the current stream by default) before this call,
+        so `hits` may still be in production there and `scores` may be a fresh
+        allocation of that stream."""
         plane = int(plane)
         _need(hits, torch.int32, "hits", self._h.device, (2,) if plane >= 0 else (3,))
         n = hits.shape[0]
@@ -359,7 +374,8 @@ class Batcher:
         _need(scores, torch.float32, "scores", self._h.device, (4,))
         req = _Request(hits.data_ptr(), n, plane, scores.data_ptr())
         ticket = ctypes.c_uint64()
-        _check(lib.pointid_batcher_submit(self.raw, ctypes.byref(req), ctypes.byref(ticket)))
+        _check(lib.pointid_batcher_submit(self.raw, ctypes.byref(req),
+                                          _stream_ptr(stream, hits.device), ctypes.byref(ticket)))
         self._live[ticket.value] = (hits, scores)
         return ticket.value
 

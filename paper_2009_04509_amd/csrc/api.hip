@@ -3,6 +3,7 @@
 // Every call only enqueues work on the caller's stream.
 #include "pointid.h"
 
+#include <algorithm>
 #include <atomic>
 #include <cstdio>
 #include <cstring>
@@ -152,7 +153,7 @@ class Workspace {
     int same = -1, ready = -1, any = -1;
     for (int i = 0; i < (int)v.size(); ++i) {
       const ScratchPool::Entry& en = v[i];
-      if (en.busy || en.bytes < bytes) continue;
+      if (en.busy || !en.ptr || en.bytes < bytes) continue;   // (empty slots are skipped)
       if (en.last == s_ || !en.used) {
         if (same < 0 || en.bytes < v[same].bytes) same = i;
       } else if (hipEventQuery(en.done) == hipSuccess) {
@@ -171,9 +172,16 @@ class Workspace {
     }
     // a new buffer, sized to the next power of two (at least 4 MiB) so that
     // requests of varying size share buffers; past 1 GiB to the next 256 MiB,
-    // so that a very large call does not reserve up to twice its need
-    v.emplace_back();
-    const int slot = (int)v.size() - 1;
+    // so that a very large call does not reserve up to twice its need.  It
+    // takes the slot of a buffer pointid_trim freed, if there is one.
+    int slot = -1;
+    for (int i = 0; i < (int)v.size() && slot < 0; ++i)
+      if (!v[i].ptr && !v[i].busy) slot = i;
+    if (slot < 0) {
+      v.emplace_back();
+      slot = (int)v.size() - 1;
+    }
+    v[slot] = ScratchPool::Entry();
     v[slot].busy = true;
     g.unlock();
     size_t cap = size_t(4) << 20;
@@ -518,6 +526,41 @@ int pointid_destroy(pointid_handle h) {
   }
   delete h;
   return POINTID_OK;
+}
+
+int pointid_trim(pointid_handle h, uint64_t keep_bytes, uint64_t* cached_bytes) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  ScratchPool* pool = h->scratch;
+  std::lock_guard<std::mutex> g(pool->mu);
+  std::vector<ScratchPool::Entry>& v = pool->entries;
+  uint64_t total = 0;
+  for (const ScratchPool::Entry& en : v) total += en.bytes;
+  // idle buffers, largest first: not being taken by a call, and their last
+  // user's work done (or never used)
+  std::vector<int> idle;
+  for (int i = 0; i < (int)v.size(); ++i) {
+    const ScratchPool::Entry& en = v[i];
+    if (!en.ptr || en.busy) continue;
+    if (!en.used || hipEventQuery(en.done) == hipSuccess) idle.push_back(i);
+  }
+  std::sort(idle.begin(), idle.end(), [&](int a, int b) { return v[a].bytes > v[b].bytes; });
+  int rc = POINTID_OK;
+  for (int i : idle) {
+    if (total <= keep_bytes) break;
+    ScratchPool::Entry& en = v[i];
+    const hipError_t e = hipFree(en.ptr);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "hipFree(scratch)");
+      break;
+    }
+    if (en.done) (void)hipEventDestroy(en.done);
+    total -= en.bytes;
+    en = ScratchPool::Entry();              // an empty slot, reused by the next allocation
+  }
+  if (cached_bytes) *cached_bytes = total;
+  return rc;
 }
 
 int pointid_precision(pointid_handle h) {

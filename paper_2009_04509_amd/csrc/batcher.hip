@@ -2,11 +2,14 @@
 // server combines requests from many clients into larger batches; §3.2
 // measures the gain) over one handle and one set of resident planes.
 //
-// Host threads submit requests and later wait for them.  A launcher thread
-// takes the pending requests in arrival order and issues them as one
-// pointid_classify_requests call on the batcher's own stream when max_requests
-// are pending or the oldest has waited max_delay_us; up to kMaxInFlight
-// batches run at once.  A completion thread waits for each batch's event in
+// Host threads submit requests and later wait for them.  A submit records an
+// event on the submitter's stream; a launcher thread takes the pending
+// requests in arrival order, makes the batcher's own stream wait for each
+// one's event (so the work the submitter enqueued before it -- the hits'
+// producer, the scores buffer's previous user -- comes first), and issues them
+// as one pointid_classify_requests call on that stream when max_requests are
+// pending or the oldest has waited max_delay_us; up to kMaxInFlight batches
+// run at once.  A completion thread waits for each batch's event in
 // launch order and wakes the requests' waiters.  Every request gets the scores
 // (bit for bit) it would get alone: batching only changes which launch
 // classifies it.
@@ -32,6 +35,7 @@ struct Pending {
   pointid_request req;
   uint64_t ticket;
   Clock::time_point arrived;
+  hipEvent_t ready;     // recorded on the submitter's stream at submit
 };
 
 struct Flight {
@@ -57,6 +61,7 @@ struct pointid_batcher_s {
   std::chrono::microseconds max_delay{0};
   hipStream_t stream = nullptr;
   std::vector<hipEvent_t> free_events;
+  std::vector<hipEvent_t> free_ready;  // submit events no pending request holds
 
   std::mutex mu;
   std::condition_variable cv_work;   // launcher: new requests, or stop
@@ -87,10 +92,12 @@ void pointid_batcher_s::launch_loop() {
       cv_work.wait_until(lk, due);
     cv_flight.wait(lk, [&] { return flight.size() < kMaxInFlight; });
     std::vector<pointid_request> batch;
+    std::vector<hipEvent_t> ready;
     const uint64_t first = pending.front().ticket;
     uint64_t last = first;
     while (!pending.empty() && (int)batch.size() < max_requests) {
       batch.push_back(pending.front().req);
+      ready.push_back(pending.front().ready);
       last = pending.front().ticket;
       pending.pop_front();
     }
@@ -98,18 +105,30 @@ void pointid_batcher_s::launch_loop() {
     free_events.pop_back();
     lk.unlock();
     Flight f{ev, first, last, POINTID_OK, {}};
-    f.status = pointid_classify_requests(h, planes.data(), (int32_t)planes.size(), batch.data(),
-                                         (int32_t)batch.size(), stream);
+    // the batch starts after what each submitter enqueued before its submit;
+    // a wait takes the event's state when it is enqueued, so the event can be
+    // recorded again at once
+    for (hipEvent_t r : ready) {
+      const hipError_t e = hipStreamWaitEvent(stream, r, 0);
+      if (e != hipSuccess && f.status == POINTID_OK) {
+        f.status = POINTID_EHIP;
+        f.msg = std::string("batch wait for a submitter's stream: ") + hipGetErrorString(e);
+      }
+    }
+    if (f.status == POINTID_OK)
+      f.status = pointid_classify_requests(h, planes.data(), (int32_t)planes.size(), batch.data(),
+                                           (int32_t)batch.size(), stream);
     if (f.status == POINTID_OK) {
       const hipError_t e = hipEventRecord(ev, stream);
       if (e != hipSuccess) {
         f.status = POINTID_EHIP;
         f.msg = std::string("batch event: ") + hipGetErrorString(e);
       }
-    } else {
+    } else if (f.msg.empty()) {
       f.msg = pointid_last_error();
     }
     lk.lock();
+    for (hipEvent_t r : ready) free_ready.push_back(r);
     flight.push_back(std::move(f));
     cv_flight.notify_all();
   }
@@ -216,12 +235,14 @@ int pointid_batcher_destroy(pointid_batcher b) {
   b->launcher.join();
   b->completer.join();
   for (hipEvent_t ev : b->free_events) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : b->free_ready) (void)hipEventDestroy(ev);   // every request was launched
   (void)hipStreamDestroy(b->stream);
   delete b;
   return POINTID_OK;
 }
 
-int pointid_batcher_submit(pointid_batcher b, const pointid_request* req, uint64_t* ticket) {
+int pointid_batcher_submit(pointid_batcher b, const pointid_request* req, void* stream,
+                           uint64_t* ticket) {
   using namespace pointid;
   if (!b || !req || !ticket) return set_error(POINTID_EINVAL, "NULL batcher, request or ticket");
   if (req->n_hits < 0) return set_error(POINTID_EINVAL, "n_hits is negative");
@@ -232,12 +253,42 @@ int pointid_batcher_submit(pointid_batcher b, const pointid_request* req, uint64
     if (reinterpret_cast<uintptr_t>(req->scores) & 15)
       return set_error(POINTID_EINVAL, "scores must be 16-byte aligned");
   }
+  // an event marking the submitter's stream here: taken from the pool, or new
+  hipEvent_t ready = nullptr;
   {
     std::lock_guard<std::mutex> lk(b->mu);
     if (b->stop) return set_error(POINTID_EINVAL, "batcher is being destroyed");
+    if (!b->free_ready.empty()) {
+      ready = b->free_ready.back();
+      b->free_ready.pop_back();
+    }
+  }
+  hipError_t e = hipSuccess;
+  if (!ready) {
+    int prev = 0;
+    e = hipGetDevice(&prev);
+    if (e == hipSuccess && prev != b->device) e = hipSetDevice(b->device);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ready, hipEventDisableTiming);
+    if (prev != b->device) (void)hipSetDevice(prev);
+  }
+  if (e == hipSuccess) e = hipEventRecord(ready, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    if (ready) {
+      std::lock_guard<std::mutex> lk(b->mu);
+      b->free_ready.push_back(ready);
+    }
+    return set_error(POINTID_EHIP, std::string("submit event: ") + hipGetErrorString(e));
+  }
+  {
+    std::lock_guard<std::mutex> lk(b->mu);
+    if (b->stop) {
+      b->free_ready.push_back(ready);
+      return set_error(POINTID_EINVAL, "batcher is being destroyed");
+    }
     try {
-      b->pending.push_back({*req, b->next_ticket, Clock::now()});
+      b->pending.push_back({*req, b->next_ticket, Clock::now(), ready});
     } catch (const std::bad_alloc&) {
+      b->free_ready.push_back(ready);
       return set_error(POINTID_ENOMEM, "host allocation failed");
     }
     *ticket = b->next_ticket++;

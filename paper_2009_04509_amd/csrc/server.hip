@@ -208,7 +208,7 @@ int pointid_server_s::handle_request(int fd, const ReqHeader& q, Buffers& buf, h
     r.plane = q.plane;
     r.scores = buf.out;
     uint64_t ticket = 0;
-    rc = pointid_batcher_submit(batcher, &r, &ticket);
+    rc = pointid_batcher_submit(batcher, &r, s, &ticket);
     if (rc == POINTID_OK) rc = pointid_batcher_wait(batcher, ticket);
   } else if (q.plane >= 0) {
     const pointid_plane& p = planes[q.plane];

@@ -125,7 +125,8 @@ def test_batcher_validation(b):
     assert L.pointid_batcher_create(FAKE, bad, 1, 64, 100, ctypes.byref(out)) == b.POINTID_EINVAL
     t = ctypes.c_uint64()
     req = R(0x3000, 5, 0, 0x4000)
-    assert L.pointid_batcher_submit(NULL, ctypes.byref(req), ctypes.byref(t)) == b.POINTID_EINVAL
+    assert L.pointid_batcher_submit(NULL, ctypes.byref(req), NULL, ctypes.byref(t)) == b.POINTID_EINVAL
+    assert L.pointid_trim(NULL, 0, None) == b.POINTID_EINVAL
     assert L.pointid_batcher_wait(NULL, 1) == b.POINTID_EINVAL
     assert L.pointid_batcher_destroy(NULL) == b.POINTID_OK
 

@@ -193,3 +193,48 @@ def test_batcher_destroy_drains(pid):
         ref = alone(pid, h, imgs, p, x)
         assert np.array_equal(sc.cpu().numpy().view(np.uint32), ref.view(np.uint32))
     h.close()
+
+
+def test_batcher_waits_for_the_submitting_stream(pid):
+    """A request's hits written on the submitting stream just before the submit
+    (behind a long queue of other work there) are the hits the batch reads:
+    the batch waits for the submitter's stream (pointid_batcher_submit's
+    `stream`), so the scores equal those of the final hits."""
+    h = pid.pointid_create(weights(), "fp16", 0)
+    imgs = [t(p.image) for p in planes()]
+    rng = np.random.default_rng(17)
+    (p, x), = make_requests(rng, [2000])
+    b = pid.Batcher(h, imgs, max_requests=1, max_delay_us=0)
+    side = torch.cuda.Stream()
+    hits = torch.zeros((len(x), 2), dtype=torch.int32, device=DEV)   # wrong hits until the copy
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        a = torch.randn((4096, 4096), device=DEV)
+        for _ in range(8):                   # keep the side stream busy for a while
+            a = a @ a
+            a = a / a.norm()
+        hits.copy_(t(x), non_blocking=True)
+        scores = torch.empty((len(x), 4), dtype=torch.float32, device=DEV)
+        ticket = b.submit(p, hits, scores, stream=side)
+    got = b.wait(ticket).cpu().numpy()
+    b.close()
+    ref = alone(pid, h, imgs, p, x)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    h.close()
+
+
+def test_trim_frees_idle_scratch(pid):
+    """pointid_trim frees the idle cached scratch; the next call allocates
+    again and gives the same bits."""
+    h = pid.pointid_create(weights(), "fp16", 0)
+    img = t(planes()[0].image)
+    hits = t(planes()[0].hits)
+    a = pid.pointid_classify(h, img, hits).cpu().numpy()
+    torch.cuda.synchronize()
+    assert pid.pointid_trim(h, 1 << 40) > 0          # a keep above the cache frees nothing
+    assert pid.pointid_trim(h, 0) == 0               # every buffer is idle after the sync
+    bb = pid.pointid_classify(h, img, hits).cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), bb.view(np.uint32))
+    torch.cuda.synchronize()
+    assert pid.pointid_trim(h, 0) == 0
+    h.close()
