@@ -14,8 +14,10 @@ the heads — over one batch of synthetic input already resident in HBM:
 
 Prints one JSON line on stdout.  `roofline` describes the kernel that takes the
 most time, timed with HIP events on its own stream inside the timed region;
-`cpu_baseline` times the fp64 CPU oracle on a bounded sample of the same
-workload on this host's cores.
+`gather_roofline` does the same for the patch gather against HBM bandwidth;
+for the event workload with a 16-bit path, `fp32` gives the same call at the
+paper's precision (fp32), timed in the same run; `cpu_baseline` times the fp64
+CPU oracle on a bounded sample of the same workload on this host's cores.
 """
 
 from __future__ import annotations
@@ -97,6 +99,8 @@ def parse():
                     help="config 3: time hit finding (pointid_find_hits) on the event's 18 "
                          "planes at threshold THR instead of classification")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fp32-block", action="store_true",
+                    help="config 3: skip timing the same call at fp32 (the paper's precision)")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 3 device-to-device copies of MIB MiB (a plain copy kernel of "
@@ -213,14 +217,30 @@ def _footprint(shapes, h3):
     return total
 
 
+def host_facts():
+    """Cores this process may run on, the BLAS thread count numpy uses, and
+    the CPU model (from /proc/cpuinfo)."""
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = None
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return cores, threads, model
+
+
 def cpu_baseline(sample, n_sample):
     import oracle
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = os.cpu_count() or 1
+    cores, threads, cpu_model = host_facts()
     w = synth.he_normal_weights()
     rng = np.random.default_rng(2024)
     if sample["kind"] == "planes":
@@ -247,7 +267,9 @@ def cpu_baseline(sample, n_sample):
         what = f"first {len(idx)} patches of the batch, oracle.classify_patches"
     dt = time.perf_counter() - t0
     return {"value": len(idx) / dt, "unit": "patches/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{what}; {dt:.1f} s", "seconds": round(dt, 2)}
+            "sample": f"{what}; {dt:.1f} s", "seconds": round(dt, 2),
+            "blas_threads": threads, "cpu_model": cpu_model,
+            "per_core": round(len(idx) / dt / cores, 2)}
 
 
 def serving(args, torch, pid, synth):
@@ -526,19 +548,15 @@ def hit_finding(args, torch, pid, synth):
                     for k, v in kern.items()},
     }
     if not args.no_cpu_baseline:
-        try:
-            from threadpoolctl import threadpool_info
-            cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            cores = 1
+        cores, _threads, cpu_model = host_facts()
         t0 = time.perf_counter()
         ref = oracle.find_hits(imgs_np, thr)
         dt = time.perf_counter() - t0
         out_json["cpu_baseline"] = {"value": round((image_bytes + 12 * len(ref)) / dt / 1e9, 3),
                                     "unit": "GB/s", "cores": 1, "kind": "oracle",
                                     "sample": f"the whole event, oracle.find_hits (numpy, one "
-                                              f"thread; {cores} BLAS threads unused); {dt:.2f} s",
-                                    "seconds": round(dt, 2)}
+                                              f"thread of the {cores} this process may use); {dt:.2f} s",
+                                    "seconds": round(dt, 2), "cpu_model": cpu_model}
         got = out[:min(n_hits, cap)].cpu().numpy()
         out_json["matches_oracle"] = bool(len(ref) == n_hits and np.array_equal(got, ref))
     h.close()
@@ -575,8 +593,49 @@ def main():
         return
     log(f"[bench] building config {args.config} workload")
     step, n, desc, sample, footprint, hit_bytes = make_workload(args, torch, pid)
-    h = pid.pointid_create(synth.he_normal_weights(), args.precision, 0)
-    log(f"[bench] warmup {args.warmup}")
+    r = measure(args, torch, pid, synth, step, n, footprint, hit_bytes, args.precision)
+    value = n / (r["ms_step"] * 1e-3)
+    total_flop = n * 2 * (CONV_MAC + FC1_MAC + TAIL_MAC)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(r["ms_step"], 4),
+        "step_ms": r["step_ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": args.precision, "data": "synthetic",
+        "config": {**desc, "precision": args.precision},
+        "roofline": r["roofline"],
+        "network_tflops": round(total_flop / (r["ms_step"] * 1e-3) / 1e12, 3),
+        "kernels": r["kernels"],
+    }
+    if "gather" in r["kern"]:
+        g = r["kern"]["gather"]
+        out["gather_roofline"] = {"kernel": "gather", "bound": "hbm", "achieved": round(g["achieved"], 2),
+                                  "peak": PEAK["hbm"], "unit": "GB/s",
+                                  "frac": round(g["achieved"] / PEAK["hbm"], 4),
+                                  "traffic": load_traffic("gather", f"config{args.config}_{args.precision}"),
+                                  "avg_launch_ms": round(g["avg_launch_ms"], 4),
+                                  "work_per_launch": g["work_per_launch"]}
+    if args.config == 3 and args.precision != "fp32" and not args.no_fp32_block:
+        # the same call at the paper's precision (fp32 operands, fp32 MFMA),
+        # timed in the same run; the headline stays the 16-bit path
+        log("[bench] the same workload at fp32")
+        r32 = measure(args, torch, pid, synth, step, n, footprint, hit_bytes, "fp32")
+        out["fp32"] = {"dtype": "fp32", "value": round(n / (r32["ms_step"] * 1e-3), 1),
+                       "unit": "patches/s", "ms_per_step": round(r32["ms_step"], 4),
+                       "step_ms": r32["step_ms"], "roofline": r32["roofline"],
+                       "kernels": r32["kernels"]}
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(sample, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+def measure(args, torch, pid, synth, step, n, footprint, hit_bytes, precision):
+    """Warm up, then time args.steps calls of `step` with a handle of
+    `precision`: per-step events on the current stream bracket the timed
+    region; the library's per-kernel events give each kernel's time."""
+    h = pid.pointid_create(synth.he_normal_weights(), precision, 0)
+    log(f"[bench] {precision}: warmup {args.warmup}")
     for _ in range(args.warmup):
         step(h)
     torch.cuda.synchronize()
@@ -601,7 +660,7 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f}; "
         f"median {np.median(per_step):.3f}, min {per_step.min():.3f}, max {per_step.max():.3f})")
 
-    patch_bytes = 9216 if args.precision == "fp32" else 4608
+    patch_bytes = 9216 if precision == "fp32" else 4608
     kern = {}
     for name, (model, _src) in KERNELS.items():
         tot, cnt = pid.pointid_timing_query(name)
@@ -630,6 +689,7 @@ def main():
                       "avg_launch_ms": tot / cnt, "achieved": rate, "unit": unit,
                       "work_per_launch": work / cnt}
         log(f"[bench] {name:10s} {tot / args.steps:8.3f} ms/step  {cnt} launches  {rate:9.2f} {unit}")
+    h.close()
 
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     d = kern[dom]
@@ -642,34 +702,18 @@ def main():
         bound, peak = "alu", PEAK["alu_fp32"]
     else:
         bound, peak = "hbm", PEAK["hbm"]
-    tag = f"config{args.config}_{args.precision}"
-    traffic = load_traffic(dom, tag)
+    tag = f"config{args.config}_{precision}"
     roof = {"kernel": dom, "bound": bound, "achieved": round(d["achieved"], 3), "peak": peak,
             "unit": d["unit"], "frac": round(d["achieved"] / peak, 4),
-            "traffic": traffic, "avg_launch_ms": round(d["avg_launch_ms"], 4),
+            "traffic": load_traffic(dom, tag), "avg_launch_ms": round(d["avg_launch_ms"], 4),
             "work_per_launch": d["work_per_launch"]}
-
-    value = n / (ms_step * 1e-3)
-    total_flop = n * 2 * (CONV_MAC + FC1_MAC + TAIL_MAC)
-    out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "step_ms": {"median": round(float(np.median(per_step)), 4),
-                    "min": round(float(per_step.min()), 4), "max": round(float(per_step.max()), 4)},
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": args.precision, "data": "synthetic",
-        "config": {**desc, "precision": args.precision},
-        "roofline": roof,
-        "network_tflops": round(total_flop / (ms_step * 1e-3) / 1e12, 3),
-        "kernels": {k: {"ms_per_step": round(v["ms_per_step"], 4), "launches": v["launches"],
-                        "achieved": round(v["achieved"], 3), "unit": v["unit"]}
-                    for k, v in kern.items()},
-    }
-    if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(sample, args.cpu_sample)
-    h.close()
-    print(json.dumps(out), flush=True)
+    return {"ms_step": ms_step,
+            "step_ms": {"median": round(float(np.median(per_step)), 4),
+                        "min": round(float(per_step.min()), 4), "max": round(float(per_step.max()), 4)},
+            "roofline": roof, "kern": kern,
+            "kernels": {k: {"ms_per_step": round(v["ms_per_step"], 4), "launches": v["launches"],
+                            "achieved": round(v["achieved"], 3), "unit": v["unit"]}
+                        for k, v in kern.items()}}
 
 
 if __name__ == "__main__":

@@ -1,4 +1,4 @@
-"""Latency model of the as-a-service deployment (paper §3.4, "Scale out
+"""Latency model of the as-a-service deployment (paper §3.3, "Scale out
 modeling", its equations for the ideal and the saturated processing time).
 
 A CPU job spends (1 - p) * t_cpu on work that stays on the CPU; the offloaded

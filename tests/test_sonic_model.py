@@ -1,4 +1,4 @@
-"""The as-a-service latency model (paper §3.4) against the numbers the paper
+"""The as-a-service latency model (paper §3.3) against the numbers the paper
 prints for it and against its own closed forms."""
 
 import json
