@@ -175,6 +175,22 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane *planes,
                             int64_t n_hits, float *scores, void *stream);
 
 /*
+ * pointid_classify_planes without any device allocation, for callers that
+ * cannot allocate (code under HIP graph capture, tight serving loops, hosts
+ * that forbid hipMalloc): the same arguments, kernels and bits, with the
+ * call's scratch (patches and split-K partials) in a fixed device array of
+ * the library (104 MiB per GPU, held from the first call on a GPU until the
+ * process ends) instead of the handle's cache.  n_hits is at most 8192.
+ * Every call on one GPU shares that array: calls that overlap on one GPU
+ * (other streams or threads) race and must be ordered by the caller.  No
+ * part of the array needs clearing between calls.
+ * Errors as pointid_classify_planes, plus EINVAL for n_hits > 8192.
+ */
+int pointid_classify_planes_noalloc(pointid_handle h, const pointid_plane *planes,
+                                    int32_t n_planes, const int32_t *hits,
+                                    int64_t n_hits, float *scores, void *stream);
+
+/*
  * Classify hits with patches whose columns span D = ticks_per_column ticks
  * each (paper §2.1: a pixel holds the charge its wire collects in the time
  * interval of its column).  Each plane is binned once into columns of D ticks

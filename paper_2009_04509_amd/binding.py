@@ -74,6 +74,8 @@ def _load():
         "pointid_classify": (cint, [vp, vp, i32, i32, vp, i64, vp, vp]),
         "pointid_classify_planes": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp, vp]),
         "pointid_classify_patches": (cint, [vp, vp, i64, vp, vp]),
+        "pointid_classify_planes_noalloc": (cint, [vp, ctypes.POINTER(_Plane), i32, vp, i64, vp,
+                                                   vp]),
         "pointid_classify_planes_ds": (cint, [vp, ctypes.POINTER(_Plane), i32, i32, vp, i64, vp,
                                               vp]),
         "pointid_downsample": (cint, [vp, i32, i32, i32, vp, vp]),
@@ -113,7 +115,8 @@ def _load():
 lib = _load()
 EXPORTED = ("pointid_create", "pointid_destroy", "pointid_precision", "pointid_trim",
             "pointid_classify",
-            "pointid_classify_planes", "pointid_classify_requests", "pointid_classify_patches",
+            "pointid_classify_planes", "pointid_classify_planes_noalloc", "pointid_classify_requests",
+            "pointid_classify_patches",
             "pointid_batcher_create", "pointid_batcher_destroy", "pointid_batcher_submit",
             "pointid_batcher_wait",
             "pointid_gather",
@@ -280,6 +283,21 @@ def pointid_classify_planes(h: Handle, images, hits: torch.Tensor,
     _need(scores, torch.float32, "scores", h.device, (4,))
     _check(lib.pointid_classify_planes(h.raw, arr, len(images), _ptr(hits), n, _ptr(scores),
                                        _stream_ptr(stream, hits.device)))
+    return scores
+
+
+def pointid_classify_planes_noalloc(h: Handle, images, hits: torch.Tensor,
+                                    scores: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """pointid_classify_planes with its scratch in the library's fixed device
+    array (at most 8192 hits; calls on one GPU must not overlap)."""
+    _need(hits, torch.int32, "hits", h.device, (3,))
+    n = hits.shape[0]
+    if scores is None:
+        scores = torch.empty((n, 4), dtype=torch.float32, device=hits.device)
+    _need(scores, torch.float32, "scores", h.device, (4,))
+    arr = _plane_array(images)
+    _check(lib.pointid_classify_planes_noalloc(h.raw, arr, len(images), _ptr(hits), n, _ptr(scores),
+                                               _stream_ptr(stream, hits.device)))
     return scores
 
 

@@ -133,6 +133,13 @@ size_t pad256(size_t b) { return (b + kScratchAlign - 1) / kScratchAlign * kScra
 class Workspace {
  public:
   Workspace(ScratchPool* pool, hipStream_t s) : pool_(pool), s_(s) {}
+  // A caller-provided buffer of `cap` bytes instead of the pool: reserve only
+  // checks the size, and nothing is allocated or recorded.
+  Workspace(void* base, size_t cap) : pool_(nullptr), s_(nullptr) {
+    fixed_ = true;
+    base_ = static_cast<char*>(base);
+    cap_ = cap;
+  }
   ~Workspace() {
     if (idx_ < 0) return;
     hipError_t e = hipEventRecord(done_, s_);
@@ -148,6 +155,7 @@ class Workspace {
 
   // Takes a buffer of at least `bytes` for this call.
   hipError_t reserve(size_t bytes) {
+    if (fixed_) return bytes <= cap_ ? hipSuccess : hipErrorInvalidValue;
     std::unique_lock<std::mutex> g(pool_->mu);
     std::vector<ScratchPool::Entry>& v = pool_->entries;
     int same = -1, ready = -1, any = -1;
@@ -208,7 +216,7 @@ class Workspace {
   hipError_t get(size_t bytes, void** out) {
     *out = nullptr;
     if (bytes == 0) return hipSuccess;
-    if (idx_ < 0 || used_ + pad256(bytes) > cap_) return hipErrorInvalidValue;
+    if ((idx_ < 0 && !fixed_) || used_ + pad256(bytes) > cap_) return hipErrorInvalidValue;
     *out = base_ + used_;
     used_ += pad256(bytes);
     return hipSuccess;
@@ -226,6 +234,7 @@ class Workspace {
 
   ScratchPool* pool_;
   hipStream_t s_;
+  bool fixed_ = false;
   int idx_ = -1;
   char* base_ = nullptr;
   size_t cap_ = 0, used_ = 0;
@@ -292,12 +301,16 @@ int run_network_16(pointid_handle h, const void* patches, bool f32_in, int64_t n
   return POINTID_OK;
 }
 
+// The hit paths: gather, then the network.  Scratch comes from the handle's
+// pool, or, when `fixed` is given, from that buffer (already sized).
 int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hits,
-                  int stride, int64_t n, float* scores, void* stream_, int tick_div = 1) {
+                  int stride, int64_t n, float* scores, void* stream_, int tick_div = 1,
+                  Workspace* fixed = nullptr) {
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   DeviceScope dev(h->device);
   if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
-  Workspace ws(h->scratch, stream);
+  Workspace pooled(h->scratch, stream);
+  Workspace& ws = fixed ? *fixed : pooled;
   hipError_t e = ws.reserve(scratch_bytes(h->precision, n, true));
   if (e != hipSuccess) return hip_fail(e, "scratch buffer");
   const bool half = h->precision != POINTID_FP32;
@@ -351,6 +364,39 @@ int classify_request_batch(pointid_handle h, const PlaneTable& planes, const Req
   if (e != hipSuccess) return hip_fail(e, "gather launch");
   if (half) return run_network_16(h, patches, false, n, nullptr, stream, ws, &reqs);
   return run_network_fp32(h, static_cast<const float*>(patches), n, nullptr, stream, ws, &reqs);
+}
+
+// ---- scratch for pointid_classify_planes_noalloc: a fixed device array,
+// sized for kNoAllocMaxHits hits at any precision (fp32 patches and the
+// split-K partials of both fused kernels, 8 splits each).  Every GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// the array's name is no device address: the address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+constexpr int64_t kNoAllocMaxHits = 8192;
+constexpr size_t kNoAllocBytes =
+    ((size_t)kNoAllocMaxHits * kPatchPix * 4 + kScratchAlign - 1) / kScratchAlign * kScratchAlign +
+    ((size_t)8 * kNoAllocMaxHits * kFc1Out * 4 + kScratchAlign - 1) / kScratchAlign * kScratchAlign;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device `dev`, looked up on
+// the first call there.
+hipError_t noalloc_scratch(int dev, void** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace
@@ -596,6 +642,33 @@ int pointid_classify_planes(pointid_handle h, const pointid_plane* planes, int32
   if (!hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
   if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
   return classify_hits(h, t, hits, 3, n_hits, scores, stream);
+}
+
+int pointid_classify_planes_noalloc(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
+                                    const int32_t* hits, int64_t n_hits, float* scores,
+                                    void* stream) {
+  if (!h) return fail(POINTID_EINVAL, "handle is NULL");
+  if (n_hits < 0) return fail(POINTID_EINVAL, "n_hits is negative");
+  if (n_hits > kNoAllocMaxHits)
+    return fail(POINTID_EINVAL, "n_hits " + std::to_string(n_hits) +
+                                    " exceeds the no-alloc scratch, which holds at most " +
+                                    std::to_string(kNoAllocMaxHits) + " hits");
+  PlaneTable t;
+  int rc = check_planes(planes, n_planes, &t);
+  if (rc != POINTID_OK) return rc;
+  if (n_hits == 0) return POINTID_OK;
+  if (!hits || !scores) return fail(POINTID_EINVAL, "NULL device pointer");
+  if (!aligned16(scores)) return fail(POINTID_EINVAL, "scores must be 16-byte aligned");
+  DeviceScope dev(h->device);
+  if (dev.error() != hipSuccess) return hip_fail(dev.error(), "hipSetDevice");
+  void* base = nullptr;
+  const hipError_t e = noalloc_scratch(h->device, &base);
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  // every byte of scratch a call reads was written earlier in the same call
+  // (patches by the gather, partials by the fused kernel), so nothing needs
+  // clearing between calls
+  Workspace ws(base, kNoAllocBytes);
+  return classify_hits(h, t, hits, 3, n_hits, scores, stream, 1, &ws);
 }
 
 int pointid_classify_planes_ds(pointid_handle h, const pointid_plane* planes, int32_t n_planes,
