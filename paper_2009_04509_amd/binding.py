@@ -16,7 +16,9 @@ import numpy as np
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libpointid.so")
+# POINTID_LIB selects another build of the same library (the sanitized host
+# builds, libpointid_asan.so / libpointid_tsan.so, for checking runs)
+LIB_PATH = os.environ.get("POINTID_LIB") or os.path.join(_PKG, "libpointid.so")
 
 POINTID_OK = 0
 POINTID_EINVAL = -1

@@ -1,9 +1,16 @@
 """Compile libpointid.so for gfx950 with hipcc (in-tree, no GPU needed).
 
-    python -m paper_2009_04509_amd.build [-v]
+    python -m paper_2009_04509_amd.build [-v] [--sanitize address|thread]
 
 Each HIP source under csrc/ is compiled to an object in csrc/_build/, then all
 objects are linked into paper_2009_04509_amd/libpointid.so.
+
+--sanitize builds a checking variant of the same library with the host code
+instrumented and the device code untouched (every -fsanitize= flag is passed
+with -Xarch_host): "address" gives libpointid_asan.so (AddressSanitizer and
+UndefinedBehaviorSanitizer, errors fatal), "thread" gives libpointid_tsan.so
+(ThreadSanitizer).  Python loads one through the POINTID_LIB environment
+variable with the matching runtime preloaded (sanitizer_runtime()).
 """
 
 from __future__ import annotations
@@ -45,25 +52,59 @@ def _run(cmd, verbose):
         print(out, flush=True)
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
+# host-only sanitizer flags: each -fsanitize= goes to the host compilation
+SANITIZE = {
+    "address": (["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer"],
+                ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined"],
+                "asan"),
+    "thread": (["-Xarch_host", "-fsanitize=thread"], ["-Xarch_host", "-fsanitize=thread"], "tsan"),
+}
+
+
+def library_path(sanitize: str | None = None) -> str:
+    return LIB if not sanitize else os.path.join(PKG, f"libpointid_{SANITIZE[sanitize][2]}.so")
+
+
+def sanitizer_runtime(sanitize: str) -> str | None:
+    """The clang runtime a process must preload to load a sanitized build."""
+    import glob
+    name = {"address": "asan", "thread": "tsan"}[sanitize]
+    llvm = os.path.join(os.path.dirname(os.path.dirname(os.path.realpath(HIPCC))), "llvm")
+    hits = sorted(glob.glob(os.path.join(llvm, "lib", "clang", "*", "lib", "linux",
+                                         f"libclang_rt.{name}-x86_64.so")))
+    return hits[-1] if hits else None
+
+
+def build(verbose: bool = False, jobs: int = 8, sanitize: str | None = None) -> str:
     """Compile every source and link the library; returns the library path."""
     if not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
-    os.makedirs(OBJDIR, exist_ok=True)
+    flags, link, objdir = FLAGS, [], OBJDIR
+    if sanitize:
+        cflags, link, tag = SANITIZE[sanitize]
+        # -O1 -g keeps the reports readable; the device code is the same
+        flags = [f for f in FLAGS if f != "-O3"] + ["-O1", "-g"] + cflags
+        objdir = os.path.join(CSRC, f"_build_{tag}")
+    out = library_path(sanitize)
+    os.makedirs(objdir, exist_ok=True)
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
+        obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        cmds.append([HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([HIPCC, *flags, "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=max(1, min(jobs, len(cmds)))) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
-    tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    shutil.move(tmp, LIB)
-    return LIB
+    tmp = out + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *link,
+          *(["-shared-libsan"] if sanitize else []), "-o", tmp, *objs], verbose)
+    shutil.move(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    path = build(verbose="-v" in sys.argv)
+    san = sys.argv[sys.argv.index("--sanitize") + 1] if "--sanitize" in sys.argv else None
+    path = build(verbose="-v" in sys.argv, sanitize=san)
     print(path)
