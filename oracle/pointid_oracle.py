@@ -385,6 +385,57 @@ def forward_mx_fp8_emulated(patches, weights) -> np.ndarray:
     return heads(h2, weights)
 
 
+def fc1_e4m3_exponents(fc1_w) -> np.ndarray:
+    """Per FC1 output n, the power-of-two exponent k_n by which an 8-bit path
+    scales column n of the FC1 weights before rounding them to e4m3: the
+    largest integer with max_k |W1[k][n]| * 2^k_n <= 448, the format's largest
+    value (0 for a column of zeros).  Exact: with max = f * 2^e, f in
+    [1/2, 1), and 448 = (7/8) * 2^9, k_n = 9 - e when f <= 7/8, else 8 - e."""
+    m = np.abs(np.asarray(fc1_w, np.float64)).max(axis=0)
+    f, e = np.frexp(m)
+    k = np.where(f <= 0.875, 9 - e, 8 - e).astype(np.float64)
+    return np.where(m > 0, k, 0.0)
+
+
+def quantize_fp8_model(weights) -> dict:
+    """Weights as the 8-bit path holds them: the conv filters rounded to fp16
+    (its conv runs as on the fp16 path), FC1 column n multiplied by 2^k_n
+    (``fc1_e4m3_exponents``) and rounded to e4m3 (``fc1_w8``, with the exponents
+    in ``fc1_exp``); everything else unchanged."""
+    q = quantize_16bit_model(weights, "fp16")
+    k = fc1_e4m3_exponents(weights["fc1_w"])
+    q["fc1_exp"] = k
+    q["fc1_w8"] = to_e4m3_rne(np.asarray(weights["fc1_w"], np.float64) * 2.0 ** k)
+    return q
+
+
+def forward_fp8_emulated(patches, weights) -> np.ndarray:
+    """The network with FC1 on e4m3 operands (the 8-bit operation of the
+    paper's outlook, section 4): the conv as on the fp16 path (fp16 patch and
+    filter, exact bias); its ReLU output through float32, then rounded to e4m3
+    (nearest even, saturating at 448); FC1 column n as ``quantize_fp8_model``
+    holds it; float64 accumulation of the e4m3 products, the sum for output n
+    multiplied by 2^-k_n, then the FC1 bias, ReLU, FC2 and the heads as given.
+    This is what the 8-bit path computes up to its accumulation order."""
+    q = quantize_fp8_model(weights)
+    P = round16(np.asarray(patches, np.float32), "fp16")
+    A = conv_relu(P, q["conv_w"], q["conv_b"])
+    A = to_e4m3_rne(A.astype(np.float32))
+    h1 = (flatten_hwc(A) @ q["fc1_w8"]) * 2.0 ** -q["fc1_exp"] + np.asarray(q["fc1_b"], np.float64)
+    h1 = np.maximum(h1, 0.0)
+    h2 = dense_relu(h1, q["fc2_w"], q["fc2_b"])
+    return heads(h2, q)
+
+
+def classify_fp8_emulated(patches, weights, chunk: int = CHUNK) -> np.ndarray:
+    """float32 [n][4] from ``forward_fp8_emulated``, chunked."""
+    patches = np.asarray(patches, dtype=np.float32).reshape(-1, PATCH, PATCH)
+    out = np.empty((patches.shape[0], 4), np.float32)
+    for s in range(0, patches.shape[0], chunk):
+        out[s:s + chunk] = forward_fp8_emulated(patches[s:s + chunk], weights).astype(np.float32)
+    return out
+
+
 def forward_bf16_emulated(patches, weights) -> np.ndarray:
     """``forward_16bit_emulated`` with bfloat16 operands."""
     return forward_16bit_emulated(patches, weights, "bf16")
