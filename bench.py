@@ -1,6 +1,6 @@
 """Benchmark: hit patches classified per second on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--precision fp32|bf16]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--precision fp32|bf16|fp16|fp8]
 
 One step is one pass of the whole hot path — patch gather, conv, FC1, FC2 and
 the heads — over one batch of synthetic input already resident in HBM:
@@ -40,13 +40,19 @@ CONV_MAC = 44 * 44 * 48 * 25            # 2,323,200
 FC1_MAC = 92928 * 128                   # 11,894,784
 TAIL_MAC = 128 * 32 + 32 * 4            # 4,224
 # MI355X published peaks.
-PEAK = {"mfma_bf16": 2500.0, "mfma_fp32": 157.3, "alu_fp32": 157.3, "hbm": 8000.0}  # TFLOP/s, GB/s
+PEAK = {"mfma_bf16": 2500.0, "mfma_fp8": 5000.0, "mfma_fp32": 157.3, "alu_fp32": 157.3,
+        "hbm": 8000.0}  # TFLOP/s, GB/s
+# The 8-bit kernel runs FC1 on e4m3 MFMAs (5.0 PFLOP/s) and the conv on fp16
+# ones (2.5): its peak is the rate at which both would finish together.
+PEAK["mfma_fp8_conv16"] = round((CONV_MAC + FC1_MAC) / (FC1_MAC / PEAK["mfma_fp8"]
+                                                       + CONV_MAC / PEAK["mfma_bf16"]), 1)
 
 # Kernel name -> (model, source file).  Model gives algorithmic work per patch.
 KERNELS = {
     "gather": ("bytes", "gather.hip"),
     "patches_to_16": ("bytes_cast", "gather.hip"),
     "conv_fc1_16": ("flops_conv_fc1", "conv_fc1_16.hip"),
+    "conv_fc1_8": ("flops_conv_fc1_8", "conv_fc1_8.hip"),
     "conv_fc1_f32": ("flops_conv_fc1_f32", "conv_fc1_f32.hip"),
     "tail": ("bytes_tail", "tail.hip"),
     "bin_ticks": ("bytes_bin", "gather.hip"),
@@ -66,7 +72,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16"])
+    ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16", "fp8"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
     ap.add_argument("--streams", type=int, default=64, help="config 5: request streams")
     ap.add_argument("--per-stream", type=int, default=32, help="config 5: requests per stream")
@@ -682,7 +688,7 @@ def measure(args, torch, pid, synth, step, n, footprint, hit_bytes, precision):
             unit, rate = "GB/s", work / (tot * 1e-3) / 1e9
         else:
             mac = {"flops_conv": CONV_MAC, "flops_fc1": FC1_MAC, "flops_conv_fc1": CONV_MAC + FC1_MAC,
-                   "flops_conv_fc1_f32": CONV_MAC + FC1_MAC}[model]
+                   "flops_conv_fc1_8": CONV_MAC + FC1_MAC, "flops_conv_fc1_f32": CONV_MAC + FC1_MAC}[model]
             work = args.steps * per_step_patches * 2 * mac
             unit, rate = "TFLOP/s", work / (tot * 1e-3) / 1e12
         kern[name] = {"ms_per_step": tot / args.steps, "launches": cnt,
@@ -696,6 +702,8 @@ def measure(args, torch, pid, synth, step, n, footprint, hit_bytes, precision):
     model = KERNELS[dom][0]
     if model == "flops_conv_fc1":
         bound, peak = "mfma", PEAK["mfma_bf16"]       # fp16 and bf16 MFMA share one peak
+    elif model == "flops_conv_fc1_8":
+        bound, peak = "mfma", PEAK["mfma_fp8_conv16"]
     elif model in ("flops_fc1", "flops_conv", "flops_conv_fc1_f32"):
         bound, peak = "mfma", PEAK["mfma_fp32"]
     elif model.startswith("flops"):

@@ -67,9 +67,17 @@ enum {
     POINTID_BF16 = 1,           /* bf16 patch, conv filter, conv output and FC1
                                    filter (round to nearest even); fp32
                                    accumulation, biases, FC2 and heads */
-    POINTID_FP16 = 2            /* as POINTID_BF16 with IEEE fp16 operands:
+    POINTID_FP16 = 2,           /* as POINTID_BF16 with IEEE fp16 operands:
                                    same MFMA rate, 3 more mantissa bits; a conv
                                    output above 65504 in magnitude overflows */
+    POINTID_FP8 = 3             /* handles only (paper §4: 8-bit operation):
+                                   the conv as POINTID_FP16; its ReLU output
+                                   (clamped to 448) and the FC1 filter rounded
+                                   to OCP e4m3, FC1 column n first multiplied
+                                   by 2^k_n, the largest power of two keeping
+                                   the column within 448, and its sums by
+                                   2^-k_n; fp32 accumulation, biases, FC2 and
+                                   heads.  Patches are made in fp16. */
 };
 
 /* Patch and network shape, paper §2.1-§2.2. */

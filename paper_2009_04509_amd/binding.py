@@ -30,6 +30,7 @@ POINTID_EIO = -6
 POINTID_FP32 = 0
 POINTID_BF16 = 1
 POINTID_FP16 = 2
+POINTID_FP8 = 3
 MAX_PLANES = 64
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ENODEV", -5: "EUNSUPPORTED",
@@ -161,7 +162,8 @@ def pointid_timing_query(kernel: str):
 
 def _precision(p) -> int:
     if isinstance(p, str):
-        return {"fp32": POINTID_FP32, "bf16": POINTID_BF16, "fp16": POINTID_FP16}[p]
+        return {"fp32": POINTID_FP32, "bf16": POINTID_BF16, "fp16": POINTID_FP16,
+                "fp8": POINTID_FP8}[p]
     return int(p)
 
 

@@ -28,7 +28,7 @@ OBJDIR = os.path.join(CSRC, "_build")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpointid.so")
 
-SOURCES = ["api.hip", "batcher.hip", "gather.hip", "conv_fc1_16.hip", "conv_fc1_f32.hip", "hits.hip",
+SOURCES = ["api.hip", "batcher.hip", "gather.hip", "conv_fc1_16.hip", "conv_fc1_8.hip", "conv_fc1_f32.hip", "hits.hip",
            "pack.hip", "server.hip", "tail.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

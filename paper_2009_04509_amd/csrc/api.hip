@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -251,7 +252,8 @@ size_t scratch_bytes(int precision, int64_t n, bool makes_patches) {
   const bool half = precision != POINTID_FP32;
   size_t b = 0;
   if (makes_patches) b += pad256((half ? 2 : 4) * (size_t)n * kPatchPix);
-  const int S = half ? conv_fc1_16_splits() : conv_fc1_f32_splits();
+  const int S = precision == POINTID_FP8 ? conv_fc1_8_splits()
+                : half ? conv_fc1_16_splits() : conv_fc1_f32_splits();
   b += pad256(sizeof(float) * (size_t)S * n * kFc1Out);
   return b;
 }
@@ -278,15 +280,25 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
   return POINTID_OK;
 }
 
-// 16-bit handles: patches (bf16 or fp16 [n][2304], or fp32 when f32_in,
-// rounded by the fused kernel) -> scores.
+// Element type of the patches a handle's network reads: 8-bit handles run
+// their conv on fp16 patches.
+int patch_dtype(int precision) { return precision == POINTID_FP8 ? POINTID_FP16 : precision; }
+
+// 16-bit and 8-bit handles: patches (bf16 or fp16 [n][2304], or fp32 when
+// f32_in, rounded by the fused 16-bit kernel) -> scores.
 int run_network_16(pointid_handle h, const void* patches, bool f32_in, int64_t n, float* scores,
                    hipStream_t stream, Workspace& ws, const RequestTable* reqs = nullptr) {
-  const int S = conv_fc1_16_splits();
+  const bool fp8 = h->precision == POINTID_FP8;
+  const int S = fp8 ? conv_fc1_8_splits() : conv_fc1_16_splits();
   float* part = nullptr;
   hipError_t e = ws.get(sizeof(float) * (size_t)S * n * kFc1Out, (void**)&part);
   if (e != hipSuccess) return hip_fail(e, "workspace (FC1 partials)");
-  {
+  if (fp8 && f32_in) return fail(POINTID_EUNSUPPORTED, "8-bit handles read 16-bit patches");
+  if (fp8) {
+    KernelTimer kt("conv_fc1_8", stream);
+    e = launch_conv_fc1_8(static_cast<const uint16_t*>(patches), n, 0, n, h->w.fc1_frag8,
+                          h->w.conv_frag, part, stream);
+  } else {
     KernelTimer kt("conv_fc1_16", stream);
     e = launch_conv_fc1_16(h->precision == POINTID_FP16, patches, f32_in, n, 0, n, h->w.fc1_frag,
                            h->w.conv_frag, part, stream);
@@ -319,7 +331,7 @@ int classify_hits(pointid_handle h, const PlaneTable& planes, const int32_t* hit
   if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
   {
     KernelTimer kt("gather", stream);
-    e = launch_gather(planes, hits, stride, n, patches, h->precision, stream, tick_div);
+    e = launch_gather(planes, hits, stride, n, patches, patch_dtype(h->precision), stream, tick_div);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
   if (half) return run_network_16(h, patches, false, n, scores, stream, ws);
@@ -359,7 +371,7 @@ int classify_request_batch(pointid_handle h, const PlaneTable& planes, const Req
   if (e != hipSuccess) return hip_fail(e, "workspace (patches)");
   {
     KernelTimer kt("gather", stream);
-    e = launch_gather_requests(planes, reqs, patches, h->precision, stream);
+    e = launch_gather_requests(planes, reqs, patches, patch_dtype(h->precision), stream);
   }
   if (e != hipSuccess) return hip_fail(e, "gather launch");
   if (half) return run_network_16(h, patches, false, n, nullptr, stream, ws, &reqs);
@@ -462,8 +474,10 @@ int pointid_create(const pointid_weights* w, int precision, int device,
                             w->fc2_b,  w->cls_w,  w->cls_b, w->mic_w, w->mic_b};
   for (const float* m : members)
     if (!m) return fail(POINTID_EINVAL, "a weight pointer is NULL");
-  if (precision != POINTID_FP32 && precision != POINTID_BF16 && precision != POINTID_FP16)
-    return fail(POINTID_EUNSUPPORTED, "precision must be POINTID_FP32, POINTID_BF16 or POINTID_FP16");
+  if (precision != POINTID_FP32 && precision != POINTID_BF16 && precision != POINTID_FP16 &&
+      precision != POINTID_FP8)
+    return fail(POINTID_EUNSUPPORTED,
+                "precision must be POINTID_FP32, POINTID_BF16, POINTID_FP16 or POINTID_FP8");
   int count = 0;
   if (hipGetDeviceCount(&count) != hipSuccess || count <= 0)
     return fail(POINTID_ENODEV, "no HIP device visible");
@@ -483,6 +497,23 @@ int pointid_create(const pointid_weights* w, int precision, int device,
   hnd->precision = precision;
   hnd->w.precision = precision;
   const bool half = precision != POINTID_FP32;
+  const bool fp8 = precision == POINTID_FP8;
+  // 8-bit handles: per FC1 output n the exponent k_n, the largest with
+  // max |W1[.][n]| 2^k_n <= 448 = (7/8) 2^9 (with max = f 2^e, f in [1/2, 1):
+  // 9 - e when f <= 7/8, else 8 - e; 0 for a column of zeros), and 2^-k_n
+  std::vector<int> fc1_exp(fp8 ? kFc1Out : 0);
+  std::vector<float> fc1_scale(fp8 ? kFc1Out : 0);
+  if (fp8) {
+    std::vector<float> mx(kFc1Out, 0.f);
+    for (int64_t k = 0; k < kFc1In; ++k)
+      for (int o = 0; o < kFc1Out; ++o) mx[o] = std::max(mx[o], std::fabs(w->fc1_w[k * kFc1Out + o]));
+    for (int o = 0; o < kFc1Out; ++o) {
+      int e2 = 0;
+      const float f = std::frexp(mx[o], &e2);
+      fc1_exp[o] = mx[o] > 0.f ? (f <= 0.875f ? 9 - e2 : 8 - e2) : 0;
+      fc1_scale[o] = std::ldexp(1.0f, -fc1_exp[o]);
+    }
+  }
 
   // one device allocation for every tensor the handle keeps
   struct Piece { const void* src; size_t bytes; const void** dst; };
@@ -497,7 +528,13 @@ int pointid_create(const pointid_weights* w, int precision, int device,
       {w->mic_w, sizeof(float) * kFc2Out, (const void**)&hnd->w.mic_w},
       {w->mic_b, sizeof(float), (const void**)&hnd->w.mic_b},
   };
-  if (half) {
+  const int* fc1_exp_dev = nullptr;
+  if (fp8) {
+    pieces.push_back({nullptr, (size_t)kConvFrags * 16, (const void**)&hnd->w.conv_frag});
+    pieces.push_back({nullptr, (size_t)kFc1Frag8Bytes, (const void**)&hnd->w.fc1_frag8});
+    pieces.push_back({fc1_scale.data(), sizeof(float) * kFc1Out, (const void**)&hnd->w.fc1_scale});
+    pieces.push_back({fc1_exp.data(), sizeof(int) * kFc1Out, (const void**)&fc1_exp_dev});
+  } else if (half) {
     pieces.push_back({nullptr, (size_t)kConvFrags * 16, (const void**)&hnd->w.conv_frag});
     pieces.push_back({nullptr, (size_t)kFc1Frags * 16, (const void**)&hnd->w.fc1_frag});
   } else {
@@ -532,7 +569,13 @@ int pointid_create(const pointid_weights* w, int precision, int device,
     e = hipMalloc(&w1, sizeof(float) * kFc1In * kFc1Out);
     if (e == hipSuccess)
       e = hipMemcpy(w1, w->fc1_w, sizeof(float) * kFc1In * kFc1Out, hipMemcpyHostToDevice);
-    if (e == hipSuccess && half)
+    if (e == hipSuccess && fp8) {
+      e = launch_pack_conv_fp16(hnd->w.conv_w, hnd->w.conv_b, const_cast<uint4*>(hnd->w.conv_frag),
+                                nullptr);
+      if (e == hipSuccess)
+        e = launch_pack_fc1_8(w1, fc1_exp_dev, const_cast<uint8_t*>(hnd->w.fc1_frag8), nullptr);
+    }
+    if (e == hipSuccess && half && !fp8)
       e = launch_pack_16(precision == POINTID_FP16, hnd->w.conv_w, hnd->w.conv_b, w1,
                          const_cast<uint4*>(hnd->w.conv_frag), const_cast<uint4*>(hnd->w.fc1_frag),
                          nullptr);
@@ -775,7 +818,7 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
   // above, a separate cast writes 16-bit patches, whose rows the fused kernel
   // then reads at half the bytes
   const bool half = h->precision != POINTID_FP32;
-  const bool cast = half && n > kInKernelCast;
+  const bool cast = half && (n > kInKernelCast || h->precision == POINTID_FP8);
   Workspace ws(h->scratch, stream);
   hipError_t e = ws.reserve(scratch_bytes(h->precision, n, cast));
   if (e != hipSuccess) return hip_fail(e, "scratch buffer");
@@ -786,7 +829,7 @@ int pointid_classify_patches(pointid_handle h, const float* patches, int64_t n,
   if (e != hipSuccess) return hip_fail(e, "workspace (16-bit patches)");
   {
     KernelTimer kt("patches_to_16", stream);
-    e = launch_patches_to_16(h->precision == POINTID_FP16, patches, n, pb, stream);
+    e = launch_patches_to_16(patch_dtype(h->precision) == POINTID_FP16, patches, n, pb, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "16-bit cast launch");
   return run_network_16(h, pb, false, n, scores, stream, ws);

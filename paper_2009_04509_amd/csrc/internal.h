@@ -40,7 +40,7 @@ struct PlaneTable {
 // Device-resident parameters of one handle.  fp32 tensors are in the ABI
 // layouts; packed tensors are in the layouts the MFMA kernels read.
 struct DeviceWeights {
-  int precision;             // POINTID_FP32 / POINTID_BF16 / POINTID_FP16
+  int precision;             // POINTID_FP32 / POINTID_BF16 / POINTID_FP16 / POINTID_FP8
   const float* conv_w;       // [48][25] fp32
   const float* conv_b;       // [48]
   const float* fc1_wt;       // [128][92928] fp32, FC1 transposed (fp32 handles)
@@ -54,7 +54,15 @@ struct DeviceWeights {
   // 16-bit handles: MFMA operand fragments (see conv_fc1_16.hip)
   const uint4* conv_frag;    // [2 shifts][3 channel tiles][64 lanes] x 8 halves
   const uint4* fc1_frag;     // [968 pairs][3 K-steps][8 output tiles][64 lanes] x 8 halves
+  // 8-bit handles (see conv_fc1_8.hip): e4m3 fragments [968 pairs][8 output
+  // tiles] x (64 lanes x 16 B, then 64 lanes x 8 B), and the factor 2^-k_n
+  // the tail multiplies FC1 output n's sums by (nullptr on other handles)
+  const uint8_t* fc1_frag8;
+  const float* fc1_scale;
 };
+
+// Bytes of the 8-bit packed FC1 weights.
+constexpr int64_t kFc1Frag8Bytes = (int64_t)(kPos / 2) * 8 * 1536;
 
 // Fragment counts of the 16-bit packed weights.
 constexpr int64_t kConvFrags = 2 * 3 * 64;
@@ -100,14 +108,22 @@ hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
                           const float* fc1_w, uint4* conv_frag, uint4* fc1_frag,
                           hipStream_t stream);
 
-// Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
-// bits, or fp32 when f32_in: rounded in the kernel) -> part[s][row0 + i][128]
-// for s < conv_fc1_16_splits().
+// The fp16 conv filter fragments alone (8-bit handles).
+hipError_t launch_pack_conv_fp16(const float* conv_w, const float* conv_b, uint4* conv_frag,
+                                 hipStream_t stream);
+// Repack fp32 FC1 weights (on the device) into the e4m3 fragments of the
+// 8-bit kernel: column n multiplied by 2^exp2[n] (exact) and rounded to e4m3.
+hipError_t launch_pack_fc1_8(const float* fc1_w, const int* exp2, uint8_t* fc1_frag8,
+                             hipStream_t stream);
+
 // Error text for pointid_last_error (this thread); returns `code`.
 int set_error(int code, const std::string& msg);
 // Device ordinal of a handle.
 int handle_device(pointid_handle h);
 
+// Fused conv + ReLU + FC1 on 16-bit MFMA: patches [n][2304] (bf16 or fp16
+// bits, or fp32 when f32_in: rounded in the kernel) -> part[s][row0 + i][128]
+// for s < conv_fc1_16_splits().
 int conv_fc1_16_splits();
 // Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
 // then n_small of 32.
@@ -115,6 +131,15 @@ void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
 hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);
+
+// Fused conv (fp16 MFMA) + ReLU + FC1 on e4m3 MFMA operands: fp16 patches
+// [n][2304] -> part[s][row0 + i][128] for s < conv_fc1_8_splits(), the sums
+// of FC1 column n still multiplied by 2^k_n.
+int conv_fc1_8_splits();
+// Tiles of the 8-bit launch for n patches on `cus` CUs (64 and 32 patches).
+void conv_fc1_8_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
+hipError_t launch_conv_fc1_8(const uint16_t* patches, int64_t n, int64_t row0, int64_t n_total,
+                             const uint8_t* w1p, const uint4* convp, float* part, hipStream_t stream);
 
 // Fused fp32 conv + ReLU + FC1 on fp32 MFMA: patches [n][2304] fp32 ->
 // part[s][row0 + i][128] for s < conv_fc1_f32_splits(), from the conv filters

@@ -1,6 +1,6 @@
-// Repacking of the fp32 conv and FC1 weights into the 16-bit MFMA operand
-// fragments read by the fused conv/FC1 kernel (layouts documented there),
-// run once per handle at create time.  Rounding uses the same hardware RNE
+// Repacking of the fp32 conv and FC1 weights into the 16-bit and 8-bit MFMA
+// operand fragments read by the fused conv/FC1 kernels (layouts documented
+// there), run once per handle at create time.  Rounding uses the same hardware RNE
 // conversion as the kernel's activations.
 #include "internal.h"
 #include "op16.h"
@@ -66,7 +66,55 @@ __global__ __launch_bounds__(64) void pack_conv_kernel(const float* __restrict__
                                    Op::pack(v[4], v[5]), Op::pack(v[6], v[7]));
 }
 
+// One thread per (fragment, lane) of the 8-bit FC1 weights: fragment
+// f = (pair P, output tile m), 1536 bytes: lane (r, g) holds, in dword d < 6,
+// the inputs of conv tile (shift d / 3, channel tile d % 3) of pair P —
+// byte e is input (2P + d / 3) * 48 + 16 (d % 3) + 4g + e of output 16m + r —
+// dwords 0-3 at byte 16 lane, dwords 4-5 at byte 1024 + 8 lane.  Each weight
+// is multiplied by 2^exp2[n] (exact) and rounded to e4m3 (nearest even; the
+// exponent keeps every product within 448, the clamp only restates it).
+__global__ __launch_bounds__(256) void pack_fc1_8_kernel(const float* __restrict__ w1,
+                                                         const int* __restrict__ exp2,
+                                                         uint8_t* __restrict__ out) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)(kPos / 2) * 8 * 64) return;
+  const int lane = (int)(idx & 63);
+  const int64_t f = idx >> 6;
+  const int m = (int)(f % 8);
+  const int64_t P = f / 8;
+  const int n = 16 * m + (lane & 15), g = lane >> 4;
+  const int k = exp2[n];
+  uint32_t d[6];
+#pragma unroll
+  for (int j = 0; j < 6; ++j) {
+    const int s = j / 3, t = j % 3;
+    const int64_t base = (2 * P + s) * kCh + 16 * t + 4 * g;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = __builtin_amdgcn_fmed3f(ldexpf(w1[(base + e) * kFc1Out + n], k), -448.f, 448.f);
+    const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+    d[j] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], lo, true);
+  }
+  uint8_t* o = out + f * 1536;
+  *reinterpret_cast<uint4*>(o + 16 * lane) = make_uint4(d[0], d[1], d[2], d[3]);
+  *reinterpret_cast<uint2*>(o + 1024 + 8 * lane) = make_uint2(d[4], d[5]);
+}
+
 }  // namespace
+
+hipError_t launch_pack_conv_fp16(const float* conv_w, const float* conv_b, uint4* conv_frag,
+                                 hipStream_t stream) {
+  pack_conv_kernel<true><<<dim3(6), dim3(64), 0, stream>>>(conv_w, conv_b, conv_frag);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_fc1_8(const float* fc1_w, const int* exp2, uint8_t* fc1_frag8,
+                             hipStream_t stream) {
+  const unsigned blocks = (unsigned)(((int64_t)(kPos / 2) * 8 * 64 + 255) / 256);
+  pack_fc1_8_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(fc1_w, exp2, fc1_frag8);
+  return hipGetLastError();
+}
 
 hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
                           const float* fc1_w, uint4* conv_frag, uint4* fc1_frag,

@@ -1,5 +1,5 @@
 // Split-K reduction of FC1 and the rest of the network (paper §2.2):
-// h1 = ReLU(b1 + sum of the FC1 partial sums), h2 = ReLU(b2 + h1 W2), then the
+// h1 = ReLU(b1 + sum of the FC1 partial sums [x 2^-k_n on 8-bit handles]), h2 = ReLU(b2 + h1 W2), then the
 // softmax branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
 // A block of 256 threads handles 32 patches.
@@ -103,6 +103,12 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
         for (int k = 0; k < kRows / 8; ++k) add4(acc[k], v[s][k]);
     }
     const float4 b = reinterpret_cast<const float4*>(w.fc1_b)[c4];
+    if (w.fc1_scale) {                       // 8-bit handles: the sums times 2^-k_n (exact)
+      const float4 sc = reinterpret_cast<const float4*>(w.fc1_scale)[c4];
+#pragma unroll
+      for (int k = 0; k < kRows / 8; ++k)
+        acc[k] = make_float4(acc[k].x * sc.x, acc[k].y * sc.y, acc[k].z * sc.z, acc[k].w * sc.w);
+    }
 #pragma unroll
     for (int k = 0; k < kRows / 8; ++k) {
       const int r = r0 + 8 * k;

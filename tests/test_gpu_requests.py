@@ -74,7 +74,7 @@ def alone(pid, h, imgs, plane, hits):
     return pid.pointid_classify_planes(h, imgs, t(hits)).cpu().numpy()
 
 
-@pytest.mark.parametrize("prec", ["fp32", "bf16", "fp16"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16", "fp16", "fp8"])
 def test_batched_requests_bitwise(pid, prec):
     h = pid.pointid_create(weights(), prec, 0)
     imgs = [t(p.image) for p in planes()]
@@ -98,6 +98,8 @@ def test_batched_requests_bitwise(pid, prec):
     got = outs[5].cpu().numpy()[idx].astype(np.float64)
     if prec == "bf16":
         ref, tol = oracle.classify_16bit_emulated(P, weights(), "bf16"), 2e-3
+    elif prec == "fp8":
+        ref, tol = oracle.classify_fp8_emulated(P, weights()), 2e-2
     else:
         ref, tol = oracle.classify_patches(P, weights()), {"fp32": 1e-4, "fp16": 2e-2}[prec]
     err = float(np.abs(got - np.asarray(ref, np.float64)).max())

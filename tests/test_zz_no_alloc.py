@@ -39,7 +39,7 @@ def event():
     return [t(p.image) for p in planes], h3
 
 
-@pytest.mark.parametrize("prec", ["fp16", "bf16", "fp32"])
+@pytest.mark.parametrize("prec", ["fp16", "bf16", "fp32", "fp8"])
 def test_noalloc_gives_the_bits_of_classify_planes(pid, event, prec):
     imgs, h3 = event
     rng = np.random.default_rng(7)
