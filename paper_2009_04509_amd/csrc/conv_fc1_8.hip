@@ -356,6 +356,12 @@ __device__ __forceinline__ void conv_fc1_8_block(
         nxt[i][3 + t] = to_e4m3x4(cB[i], nxt[i][3 + t]);
       }
     };
+    // Wave priorities stepped down through the step: the two waves of a SIMD
+    // run the same sequence, and the arbiter favours the older one, so without
+    // this the younger one finished each step about a quarter of a step later
+    // (alone on the SIMD, its conversions no longer hidden behind MFMAs);
+    // a wave past a checkpoint yields to one that has not reached it.
+    __builtin_amdgcn_s_setprio(3);
     own_m(0);
     __builtin_amdgcn_sched_barrier(0);
     fix_win(win);
@@ -363,6 +369,7 @@ __device__ __forceinline__ void conv_fc1_8_block(
     __builtin_amdgcn_sched_barrier(0);
     own_m(1);
     __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(2);
     conv_quant(0);
     conv_issue(1);
     __builtin_amdgcn_sched_barrier(0);
@@ -370,6 +377,7 @@ __device__ __forceinline__ void conv_fc1_8_block(
     __builtin_amdgcn_sched_barrier(0);
     own_m(2);
     __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(1);
     conv_quant(1);
     conv_issue(2);
     __builtin_amdgcn_sched_barrier(0);
@@ -377,6 +385,7 @@ __device__ __forceinline__ void conv_fc1_8_block(
     __builtin_amdgcn_sched_barrier(0);
     own_m(3);
     __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
     conv_quant(2);
     __builtin_amdgcn_sched_barrier(0);
     oth_m(2);
