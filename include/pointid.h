@@ -121,9 +121,12 @@ typedef struct {
 
 /*
  * Create a classifier on `device` (HIP ordinal) computing in `precision`
- * (POINTID_FP32, POINTID_BF16 or POINTID_FP16).  The weights are converted and repacked into
- * device memory owned by the handle; the call is synchronous, so the host
- * weights may be freed when it returns.
+ * (POINTID_FP32, POINTID_BF16, POINTID_FP16 or POINTID_FP8).  The weights are
+ * converted and repacked into device memory owned by the handle (POINTID_FP8:
+ * the per-column exponents k_n are taken from the fp32 FC1 weights on the
+ * host, a column whose largest magnitude is below about 2^-117 loses its
+ * contribution to fp32 underflow in the 2^-k_n factor); the call is
+ * synchronous, so the host weights may be freed when it returns.
  * Errors: EINVAL (NULL w, NULL member, NULL out), EUNSUPPORTED (precision),
  * ENODEV (no such device, or not gfx950), ENOMEM, EHIP.  *out is set to NULL
  * on failure.
@@ -289,6 +292,9 @@ int pointid_batcher_wait(pointid_batcher b, uint64_t ticket);
  * batches of ready patches).
  *   patches device fp32 [n][48][48] (row = wire, column = tick), 16-byte aligned
  *   scores  device fp32 [n][4], 16-byte aligned
+ * 16-bit and 8-bit handles round the patches to their 16-bit type first
+ * (8-bit handles: fp16), inside the fused kernel for up to 4,096 patches on
+ * 16-bit handles, else in a separate pass.
  * Errors: EINVAL (NULL handle, n < 0, NULL or misaligned pointer with n > 0),
  * ENOMEM, EHIP.
  */
