@@ -124,8 +124,8 @@ typedef struct {
  * (POINTID_FP32, POINTID_BF16, POINTID_FP16 or POINTID_FP8).  The weights are
  * converted and repacked into device memory owned by the handle (POINTID_FP8:
  * the per-column exponents k_n are taken from the fp32 FC1 weights on the
- * host, a column whose largest magnitude is below about 2^-117 loses its
- * contribution to fp32 underflow in the 2^-k_n factor); the call is
+ * host; the factor 2^-k_n is an fp32 value, subnormal for a column whose
+ * largest magnitude is below 2^-118 and zero below 2^-141); the call is
  * synchronous, so the host weights may be freed when it returns.
  * Errors: EINVAL (NULL w, NULL member, NULL out), EUNSUPPORTED (precision),
  * ENODEV (no such device, or not gfx950), ENOMEM, EHIP.  *out is set to NULL
