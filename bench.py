@@ -417,18 +417,21 @@ def serving(args, torch, pid, synth):
     # streams at once their launches overlap, and the step's wall clock is the
     # time base instead.
     roof = None
-    if "conv_fc1_16" in kern:
+    fused = [(k, pk) for k, pk in (("conv_fc1_16", "mfma_bf16"), ("conv_fc1_8", "mfma_fp8_conv16"),
+                                    ("conv_fc1_f32", "mfma_fp32")) if k in kern]
+    if fused:
+        fk, pk = fused[0]
         one_stream = batcher is not None or (server is not None and K > 0)
         flop = total * args.steps * 2 * (CONV_MAC + FC1_MAC)
-        base_s = (kern["conv_fc1_16"]["ms_per_step"] * args.steps * 1e-3 if one_stream else wall)
+        base_s = (kern[fk]["ms_per_step"] * args.steps * 1e-3 if one_stream else wall)
         ach = flop / base_s / 1e12
-        roof = {"kernel": "conv_fc1_16", "bound": "mfma", "achieved": round(ach, 3),
-                "peak": PEAK["mfma_bf16"], "unit": "TFLOP/s",
-                "frac": round(ach / PEAK["mfma_bf16"], 4), "traffic": None,
+        roof = {"kernel": fk, "bound": "mfma", "achieved": round(ach, 3),
+                "peak": PEAK[pk], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK[pk], 4), "traffic": None,
                 "time_base": "launch events on the batcher's stream" if one_stream else
                              "wall clock of the steps (launches on many streams overlap)",
-                "avg_launch_ms": kern["conv_fc1_16"]["avg_launch_ms"],
-                "work_per_launch": flop / kern["conv_fc1_16"]["launches"]}
+                "avg_launch_ms": kern[fk]["avg_launch_ms"],
+                "work_per_launch": flop / kern[fk]["launches"]}
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "patches/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,

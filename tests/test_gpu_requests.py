@@ -125,7 +125,7 @@ def test_more_than_64_requests(pid):
     h.close()
 
 
-@pytest.mark.parametrize("prec", ["bf16", "fp16"])
+@pytest.mark.parametrize("prec", ["bf16", "fp16", "fp8"])
 def test_batcher_threads_bitwise(pid, prec):
     """Requests submitted from 4 host threads through the dynamic batcher get
     the bits they get alone."""
