@@ -105,6 +105,7 @@ def parse():
                     help="config 3: time hit finding (pointid_find_hits) on the event's 18 "
                          "planes at threshold THR instead of classification")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-h2d", action="store_true", help="skip timing the host-to-device copies")
     ap.add_argument("--no-fp32-block", action="store_true",
                     help="config 3: skip timing the same call at fp32 (the paper's precision)")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
@@ -275,7 +276,48 @@ def cpu_baseline(sample, n_sample):
     return {"value": len(idx) / dt, "unit": "patches/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{what}; {dt:.1f} s", "seconds": round(dt, 2),
             "blas_threads": threads, "cpu_model": cpu_model,
-            "per_core": round(len(idx) / dt / cores, 2)}
+            "per_core": round(len(idx) / dt / cores, 2),
+            "paper_context": "paper section 3.1: 213 s of single-process TensorFlow inference "
+                             "for about 55,000 patches per event, about 258 patches/s per process "
+                             "(other hardware; context only)"}
+
+
+def transfer(args, torch, sample, n):
+    """Host-to-device copies from pinned host memory, outside the timed region:
+    the event's planes and hits (what this library's hit paths read), and the
+    same hits' pre-cut fp32 patches (what the paper's clients transmit, its
+    t_transmit).  Median of 5 copies each, HIP events on the current stream."""
+    def time_copy(nbytes):
+        src = torch.empty(nbytes // 4, dtype=torch.float32, pin_memory=True)
+        dst = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        ms = []
+        for _ in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dst.copy_(src, non_blocking=True)
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        del src, dst
+        return float(np.median(ms[1:]))
+    if sample["kind"] == "planes":
+        in_bytes = sum(im.nbytes for im in sample["images"]) + sample["hits"].nbytes
+    elif sample["kind"] == "plane":
+        in_bytes = sample["image"].nbytes + sample["hits"].nbytes
+    else:
+        in_bytes = 0
+    out = {"note": "host-to-device copies from pinned memory, not in the timed region; "
+                   "the analogue of the paper's t_transmit"}
+    if in_bytes:
+        ms = time_copy(in_bytes)
+        out["planes_and_hits"] = {"bytes": int(in_bytes), "ms": round(ms, 4),
+                                  "GB_per_s": round(in_bytes / (ms * 1e-3) / 1e9, 2)}
+    pb = n * 9216
+    ms = time_copy(pb)
+    out["precut_fp32_patches"] = {"bytes": int(pb), "ms": round(ms, 4),
+                                  "GB_per_s": round(pb / (ms * 1e-3) / 1e9, 2)}
+    log(f"[bench] H2D: {out}")
+    return out
 
 
 def serving(args, torch, pid, synth):
@@ -633,6 +675,8 @@ def main():
                        "unit": "patches/s", "ms_per_step": round(r32["ms_step"], 4),
                        "step_ms": r32["step_ms"], "roofline": r32["roofline"],
                        "kernels": r32["kernels"]}
+    if not args.no_h2d and args.config in (2, 3):
+        out["h2d"] = transfer(args, torch, sample, n)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(sample, args.cpu_sample)
