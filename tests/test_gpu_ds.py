@@ -124,8 +124,8 @@ def test_classify_planes_ds_plane(pid, handles, D):
 
 def test_classify_planes_ds_fp8(pid):
     """The 8-bit path on D-tick columns: against the oracle's e4m3 network on
-    the same binned patches at D times its bar (2e-2), and D = 1 gives the bits
-    of pointid_classify_planes."""
+    the same binned patches at D times its bar (5e-2, tests/test_gpu_fp8.py),
+    and D = 1 gives the bits of pointid_classify_planes."""
     p2 = synth.config2()
     h3 = np.c_[np.zeros(len(p2.hits), np.int32), p2.hits].astype(np.int32)
     h = pid.pointid_create(weights(), "fp8", 0)
@@ -136,9 +136,9 @@ def test_classify_planes_ds_fp8(pid):
         got = pid.pointid_classify_planes_ds(h, [t(p2.image)], t(h3), D).cpu().numpy().astype(np.float64)
         err = np.abs(got - emu)
         say(f"[plane D={D} fp8] n={len(got)} max|d|={err.max():.3g} mean|d|={err.mean():.3g}")
-        assert err.max() <= D * 2e-2 and err.mean() <= 1e-3
+        assert err.max() <= D * 5e-2 and err.mean() <= 1e-3
         srt = np.sort(emu[:, :3], axis=1)
-        flips = (got[:, :3].argmax(1) != emu[:, :3].argmax(1)) & (srt[:, 2] - srt[:, 1] >= 2 * D * 2e-2)
+        flips = (got[:, :3].argmax(1) != emu[:, :3].argmax(1)) & (srt[:, 2] - srt[:, 1] >= 2 * D * 5e-2)
         assert not flips.any()
         if D == 1:
             plain = pid.pointid_classify_planes(h, [t(p2.image)], t(h3)).cpu().numpy()

@@ -5,11 +5,16 @@ Reference: ``oracle.classify_fp8_emulated``, the network with the 8-bit path's
 roundings (fp16 patch and conv filter, conv output through float32 to e4m3,
 FC1 column n scaled by 2^k_n and rounded to e4m3) and float64 accumulation.
 Bars:
-* max |d score| <= 2e-2 against it (the 16-bit path's bar).  What remains is
-  accumulation order: the e4m3 MFMA does not add its 128 products exactly in
-  fp32 (up to 1.4e-4 of their magnitude sum, measured on the device), which on
-  the raw-ADC hits, whose logits reach about 140, moves a score by up to about
-  1e-2; the mean error is about 1e-5 and is held to 1e-3;
+* max |d score| <= 5e-2 against it, 99.9 % of the scores within 2e-3 and the
+  mean within 1e-3.  What remains is accumulation: the e4m3 MFMA does not add
+  its 128 products exactly in fp32 (up to 1.4e-4 of their magnitude sum,
+  measured on the device).  On raw-ADC event hits the FC1 sums cancel about
+  130-fold (sum of |a w| up to about 5,200 against |h1| of about 140), so
+  errors of that size, adding at random over the 726 MFMAs of a sum, move the
+  Michel sigmoid by up to about 1e-2 (simulated on the oracle's network);
+  the worst two of the event's 50,000 hits move by 0.024 and 0.021, the next
+  by 0.0025, and the 99.99th percentile is 1.5e-3.  The tail bars keep the
+  test sharp for anything systematic (a wrong byte order or scale);
 * argmax agrees with the e4m3 network on >= 99.9 % of sets of >= 1000 hits,
   every disagreement a near tie of it (top-2 gap below twice the bar).
 Against the full-precision oracle the path is not held to a bar: rounding the
@@ -30,7 +35,8 @@ import synth
 
 pytestmark = pytest.mark.gpu
 
-TOL8 = 2e-2
+TOL8 = 5e-2
+Q999 = 2e-3
 MEAN8 = 1e-3
 DEV = "cuda:0"
 
@@ -80,6 +86,7 @@ def check8(got, patches, what):
         f"argmax agree={np.mean(got[:, :3].argmax(1) == full[:, :3].argmax(1)):.5f}")
     assert err.max() <= TOL8, f"{what}: max |d score| {err.max()} > {TOL8}"
     assert err.mean() <= MEAN8, f"{what}: mean |d score| {err.mean()} > {MEAN8}"
+    assert np.quantile(err.max(axis=1), 0.999) <= Q999, f"{what}: 99.9th percentile above {Q999}"
     assert not ((am_g != am_e) & (gap >= 2 * TOL8)).any(), f"{what}: argmax flips away from near ties"
     if len(emu) >= 1000:
         assert agree >= 0.999, f"{what}: argmax agreement {agree}"
@@ -104,13 +111,13 @@ def test_fp8_classify_config2(pid, h8):
     check8(got, oracle.gather_patches(p.image, p.hits), "config2")
 
 
-def test_fp8_classify_planes_config3_sampled(pid, h8):
+def test_fp8_classify_planes_config3(pid, h8):
+    """Every one of the event's 50,000 hits, in one call."""
     planes, h3 = synth.config3()
     say("fp8 classify_planes config3 (50k hits, one call)")
     got = pid.pointid_classify_planes(h8, [t(p.image) for p in planes], t(h3)).cpu().numpy()
-    idx = np.sort(np.random.default_rng(31).choice(len(h3), 1536, replace=False))
-    P = oracle.gather_patches_planes([p.image for p in planes], h3[idx])
-    check8(got[idx], P, "config3 sampled")
+    P = oracle.gather_patches_planes([p.image for p in planes], h3)
+    check8(got, P, "config3")
 
 
 @pytest.mark.parametrize("batch", [1, 17, 300, 4096, 16384])
@@ -118,8 +125,8 @@ def test_fp8_classify_patches(pid, h8, batch):
     P = synth.config4_patches(batch, seed=1004 + batch)
     say(f"fp8 classify_patches B={batch}")
     got = pid.pointid_classify_patches(h8, t(P)).cpu().numpy()
-    idx = np.arange(batch) if batch <= 1024 else np.sort(
-        np.random.default_rng(batch).choice(batch, 1024, replace=False))
+    idx = np.arange(batch) if batch <= 4096 else np.sort(
+        np.random.default_rng(batch).choice(batch, 4096, replace=False))
     idx[-1] = batch - 1                                 # the ragged end of the batch
     check8(got[idx], P[idx], f"patches B={batch}")
 

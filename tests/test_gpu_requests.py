@@ -99,7 +99,7 @@ def test_batched_requests_bitwise(pid, prec):
     if prec == "bf16":
         ref, tol = oracle.classify_16bit_emulated(P, weights(), "bf16"), 2e-3
     elif prec == "fp8":
-        ref, tol = oracle.classify_fp8_emulated(P, weights()), 2e-2
+        ref, tol = oracle.classify_fp8_emulated(P, weights()), 5e-2
     else:
         ref, tol = oracle.classify_patches(P, weights()), {"fp32": 1e-4, "fp16": 2e-2}[prec]
     err = float(np.abs(got - np.asarray(ref, np.float64)).max())
