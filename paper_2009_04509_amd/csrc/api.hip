@@ -92,7 +92,10 @@ Timing& timing() {
   return t;
 }
 
-// Brackets one launch with events on its stream while timing is enabled.
+// Brackets the launch in its scope with events on its stream while timing is
+// enabled.  (Events attached to the dispatch itself, through
+// hipExtLaunchKernel, would drop the two markers, but cost the host about
+// 25 us per launch: the host, not the GPU, then sets the pace of small calls.)
 class KernelTimer {
  public:
   KernelTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
@@ -143,7 +146,7 @@ class Workspace {
   }
   ~Workspace() {
     if (idx_ < 0) return;
-    hipError_t e = hipEventRecord(done_, s_);
+    hipError_t e = recorded_ ? hipSuccess : hipEventRecord(done_, s_);
     // without the event, the next user could not tell when this call's work
     // is done: wait for it here (an error path only)
     if (e != hipSuccess) (void)hipStreamSynchronize(s_);
@@ -213,6 +216,18 @@ class Workspace {
     return hipSuccess;
   }
 
+  // Lets the calling thread's next launch record the completion event at the
+  // end of its kernel (no packet of its own on the stream); false for a
+  // caller's buffer, which has no event.
+  bool attach_done() {
+    if (fixed_ || idx_ < 0) return false;
+    LaunchEvents& ev = launch_events();
+    if (ev.stop) return false;
+    ev.stop = done_;
+    return true;
+  }
+  void mark_recorded() { recorded_ = true; }
+
   // Carves the next piece (256-byte aligned) out of the reserved buffer.
   hipError_t get(size_t bytes, void** out) {
     *out = nullptr;
@@ -236,10 +251,28 @@ class Workspace {
   ScratchPool* pool_;
   hipStream_t s_;
   bool fixed_ = false;
+  bool recorded_ = false;
   int idx_ = -1;
   char* base_ = nullptr;
   size_t cap_ = 0, used_ = 0;
   hipEvent_t done_ = nullptr;
+};
+
+// Scope of a call's last launch: the launch also records the workspace's
+// completion event.
+class EndsCall {
+ public:
+  explicit EndsCall(Workspace& ws) : ws_(ws), on_(ws.attach_done()) {}
+  ~EndsCall() {
+    if (on_) launch_events().stop = nullptr;
+  }
+  void launched(hipError_t e) {
+    if (on_ && e == hipSuccess && launch_events().stop == nullptr) ws_.mark_recorded();
+  }
+
+ private:
+  Workspace& ws_;
+  bool on_;
 };
 
 // Pre-cut fp32 batches up to this size are rounded to 16 bits inside the
@@ -273,8 +306,10 @@ int run_network_fp32(pointid_handle h, const float* patches, int64_t n, float* s
   if (e != hipSuccess) return hip_fail(e, "conv_fc1_f32 launch");
   {
     KernelTimer kt("tail", stream);
+    EndsCall end(ws);
     e = reqs ? launch_tail_requests(part, S, h->w, *reqs, stream)
              : launch_tail(part, S, n, h->w, scores, stream);
+    end.launched(e);
   }
   if (e != hipSuccess) return hip_fail(e, "tail launch");
   return POINTID_OK;
@@ -306,8 +341,10 @@ int run_network_16(pointid_handle h, const void* patches, bool f32_in, int64_t n
   if (e != hipSuccess) return hip_fail(e, "conv_fc1 launch");
   {
     KernelTimer kt("tail", stream);
+    EndsCall end(ws);
     e = reqs ? launch_tail_requests(part, S, h->w, *reqs, stream)
              : launch_tail(part, S, n, h->w, scores, stream);
+    end.launched(e);
   }
   if (e != hipSuccess) return hip_fail(e, "tail launch");
   return POINTID_OK;
@@ -414,6 +451,10 @@ hipError_t noalloc_scratch(int dev, void** out) {
 }  // namespace
 
 namespace pointid {
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
 int set_error(int code, const std::string& msg) { return fail(code, msg); }
 int handle_device(pointid_handle h) { return h->device; }
 }  // namespace pointid

@@ -7,7 +7,8 @@
 // operand producer: the maps exist only in registers.
 //
 // Work split.  A block owns 96 patches (32 in the blocks that finish a batch:
-// see conv_fc1_16_tiles) and one of kSplits contiguous ranges of
+// see conv_fc1_16_tiles; small batches run the thin tiles further below, with
+// the same sums) and one of kSplits contiguous ranges of
 // map positions (split-K); blockIdx % 8 selects the range, so every block on one
 // XCD reads the same 1/8 of the FC1 weights and that slice (2.97 MB) stays in
 // the XCD's 4 MB L2.  Positions are taken in pairs (x, x+1) with x even: the
@@ -455,6 +456,236 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
                                                    patches, n, w1p, convp, part, row0, n_total);
 }
 
+
+// ---- Thin tiles: batches that leave most of the chip idle.  Then one block's
+// K-loop is the whole call, and the barrier per K-step and the swap through
+// LDS are latency, not throughput.  A thin block holds 16 or 32 patches (1 or
+// 2 MFMA patch tiles) with the same 8 waves (position group x output half);
+// each wave computes the conv of every tile of the block (the two output
+// halves of a position group both compute it: twice the conv MFMAs, on a chip
+// that is mostly idle) and feeds it to its own FC1 MFMAs, so no fragment
+// crosses waves.  All input rows of the block's position range (at most 11)
+// are staged in LDS once, so the loop has no barrier.  Every FC1 accumulator
+// sees the same operands in the same order as in the tiles above, and the
+// reduction over position groups is the same: a patch's sums are bit for bit
+// those of the other tile shapes.
+constexpr int kThinRows = 11;                 // input rows of one position range, at most
+template <int kBt>
+struct Thin {
+  static constexpr int kTiles = kBt / 16;
+  static constexpr int kSlot = kBt * kRP;                  // dwords per staged row
+  static constexpr int kRegion = kMT * kTiles * 4 * 64;    // one wave's partial sums
+  // one row slot more than a range needs: the loop reads the window of the
+  // pair after its last one (the result is never used), which may lie one row lower
+  static constexpr int kRowsDw = (kThinRows + 1) * kSlot;
+  static constexpr int kLdsDwords = kRowsDw > 4 * kRegion ? kRowsDw : 4 * kRegion;
+  static constexpr int kRowChunks = kBt * 6;               // 16 B chunks per staged row
+  static constexpr int kPer = (kThinRows * kRowChunks + kThreads - 1) / kThreads;
+  static_assert(kTiles >= 1 && kTiles <= 2, "1 or 2 patch tiles");
+};
+
+// input rows a position range spans, at most, over the ranges of `splits`
+constexpr int thin_rows_needed(int splits) {
+  int most = 0;
+  for (int s = 0; s < splits; ++s) {
+    const int g0 = (kPos / 2 / kKGroups) * s / splits;
+    const int g1 = (kPos / 2 / kKGroups) * (s + 1) / splits;
+    const int rows = (kKGroups * g1 - 1) / kPairsPerRow + kK - (kKGroups * g0) / kPairsPerRow;
+    most = rows > most ? rows : most;
+  }
+  return most;
+}
+
+template <bool kFp16, int kSplits, int kBt, class In>
+__device__ __forceinline__ void thin_block(
+    uint32_t* lds, int split, int64_t p_base, const In* __restrict__ patches, int64_t n,
+    const uint4* __restrict__ w1p, const uint4* __restrict__ convp, float* __restrict__ part,
+    int64_t row0, int64_t n_total) {
+  using T = Thin<kBt>;
+  constexpr int kTiles = T::kTiles, kSlot = T::kSlot, kRegion = T::kRegion;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave % kKGroups;
+  const int nh = wave / kKGroups;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+  constexpr int kGroups = kPos / 2 / kKGroups;
+  const int G0 = (kGroups * split) / kSplits;
+  const int steps = (kGroups * (split + 1)) / kSplits - G0;
+  const int P0 = kKGroups * G0;
+  const int r0 = P0 / kPairsPerRow;                        // first input row of the range
+  const int nrows = (P0 + kKGroups * steps - 1) / kPairsPerRow + kK - r0;
+  using Op = Op16<kFp16>;
+
+  // ---- every input row of the range, all loads in flight together
+  {
+    const int total = nrows * T::kRowChunks;
+    uint4 v[T::kPer];
+#pragma unroll
+    for (int k = 0; k < T::kPer; ++k) {
+      const int c = tid + k * kThreads;
+      if (c < total) {
+        const int j = c / T::kRowChunks;
+        v[k] = row_chunk_load<kBt, kFp16, In>(patches, n, p_base, r0 + j, c - j * T::kRowChunks);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < T::kPer; ++k) {
+      const int c = tid + k * kThreads;
+      if (c < total) {
+        const int j = c / T::kRowChunks, cc = c - j * T::kRowChunks;
+        const int p = cc / 6, h = cc - (cc / 6) * 6;
+        uint32_t* d = lds + j * kSlot + p * kRP + h * 4;
+        *reinterpret_cast<uint2*>(d) = make_uint2(v[k].x, v[k].y);
+        *reinterpret_cast<uint2*>(d + 2) = make_uint2(v[k].z, v[k].w);
+      }
+    }
+  }
+  // the six conv filter fragments [shift][channel tile], kept in registers:
+  // K-step q uses fragments 2q and 2q + 1
+  uint4 filt[6];
+#pragma unroll
+  for (int k = 0; k < 6; ++k) filt[k] = convp[k * 64 + lane];
+
+  int woff[4], wrow[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    int f = 8 * grp + 2 * d;
+    if (f > 28) f = 28;                      // slots 30-31 are constants (set below)
+    wrow[d] = f / 6 - r0;
+    woff[d] = (f % 6) / 2 + col * kRP;
+  }
+  const bool const_slot = (grp == 3);
+  auto read_win = [&](int P, uint4 (&win)[kTiles]) {
+    const int y = P / kPairsPerRow;
+    const int xh = P - y * kPairsPerRow;
+    int base[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) base[d] = (y + wrow[d]) * kSlot + woff[d] + xh;
+#pragma unroll
+    for (int i = 0; i < kTiles; ++i) {
+      const int o = i * 16 * kRP;
+      win[i].x = lds[base[0] + o];
+      win[i].y = lds[base[1] + o];
+      win[i].z = lds[base[2] + o];
+      win[i].w = const_slot ? Op::kOnes : lds[base[3] + o];
+    }
+  };
+  auto convert1 = [&](const floatx4& ca, const floatx4& cb) {
+    return make_uint4(relu2(Op::pack(ca[0], ca[1])), relu2(Op::pack(ca[2], ca[3])),
+                      relu2(Op::pack(cb[0], cb[1])), relu2(Op::pack(cb[2], cb[3])));
+  };
+  const __amdgpu_buffer_rsrc_t w1r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(w1p), (short)0, (int)(kFc1Frags * 16), 0x00020000);
+  const int voff = lane * 16 + nh * kMT * 1024;
+  auto load_one = [&](int P, int q, int m) {
+    return __builtin_bit_cast(
+        uint4, __builtin_amdgcn_raw_buffer_load_b128(w1r, voff + m * 1024, (P * 3 + q) * 8 * 1024, 0));
+  };
+
+  floatx4 acc[kMT][kTiles];
+#pragma unroll
+  for (int m = 0; m < kMT; ++m)
+#pragma unroll
+    for (int i = 0; i < kTiles; ++i) acc[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
+  // FC1 weights: 3 register sets, set q for K-step q of a pair, each reloaded
+  // for the next pair as soon as its MFMAs have issued (three K-steps ahead:
+  // with one or two patch tiles a K-step is short)
+  uint4 w[3][kMT], win[kTiles], own[kTiles];
+#pragma unroll
+  for (int m = 0; m < kMT; ++m) {
+    w[0][m] = load_one(P0 + kg, 0, m);
+    w[1][m] = load_one(P0 + kg, 1, m);
+    w[2][m] = load_one(P0 + kg, 2, m);
+  }
+  __syncthreads();                           // the staged rows
+  const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+  read_win(P0 + kg, win);
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i) own[i] = convert1(Op::mfma(filt[0], win[i], z), Op::mfma(filt[1], win[i], z));
+
+#pragma unroll 1
+  for (int step = 0; step < steps; ++step) {
+    const int P = P0 + kKGroups * step + kg;
+    uint4 win_next[kTiles];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const int nq = (q + 1) % 3;            // the next K-step
+      // FC1 of K-step q (past the end of the weights the reload reads 0)
+#pragma unroll
+      for (int m = 0; m < kMT; ++m) {
+#pragma unroll
+        for (int i = 0; i < kTiles; ++i) acc[m][i] = Op::mfma(w[q][m], own[i], acc[m][i]);
+        w[q][m] = load_one(P + kKGroups, q, m);
+      }
+      // conv of the next K-step (its window: this pair's, or the next pair's
+      // after the last K-step)
+      if (q == 1) read_win(P + kKGroups, win_next);
+#pragma unroll
+      for (int i = 0; i < kTiles; ++i) {
+        const uint4& wi = (q == 2) ? win_next[i] : win[i];
+        own[i] = convert1(Op::mfma(filt[2 * nq], wi, z), Op::mfma(filt[2 * nq + 1], wi, z));
+      }
+      if (q == 2) {
+#pragma unroll
+        for (int i = 0; i < kTiles; ++i) win[i] = win_next[i];
+      }
+    }
+  }
+
+  // ---- the fixed-order reduction of the tiles above: (g0 + g2) + (g1 + g3)
+  __syncthreads();                           // every wave is done with the rows
+  floatx4* red = reinterpret_cast<floatx4*>(lds);
+  auto slot = [&](int region, int m, int i) {
+    return region * (kRegion / 4) + (m * kTiles + i) * 64 + lane;
+  };
+  auto put = [&](int region) {
+#pragma unroll
+    for (int m = 0; m < kMT; ++m)
+#pragma unroll
+      for (int i = 0; i < kTiles; ++i) red[slot(region, m, i)] = acc[m][i];
+  };
+  auto add = [&](int region) {
+#pragma unroll
+    for (int m = 0; m < kMT; ++m)
+#pragma unroll
+      for (int i = 0; i < kTiles; ++i) acc[m][i] += red[slot(region, m, i)];
+  };
+  if (kg >= 2) put(nh * 2 + (kg - 2));
+  __syncthreads();
+  if (kg < 2) add(nh * 2 + kg);
+  __syncthreads();
+  if (kg == 1) put(nh);
+  __syncthreads();
+  if (kg != 0) return;
+  add(nh);
+
+  float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i) {
+    const int64_t po = (int64_t)i * 16 + col;
+#pragma unroll
+    for (int m = 0; m < kMT; ++m) {
+      const int o = 16 * (nh * kMT + m) + 4 * grp;
+      if (p_base + po < n)
+        __builtin_nontemporal_store(acc[m][i], reinterpret_cast<floatx4*>(dst + po * kFc1Out + o));
+    }
+  }
+}
+
+template <bool kFp16, int kSplits, int kBt, class In>
+__global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_thin_kernel(
+    const In* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
+    const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
+  static_assert(thin_rows_needed(kSplits) <= kThinRows, "a position range's rows fit the stage");
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Thin<kBt>::kLdsDwords];
+  const int split = blockIdx.x % kSplits;
+  const int64_t t = blockIdx.x / kSplits;
+  thin_block<kFp16, kSplits, kBt, In>(lds, split, t * kBt, patches, n, w1p, convp, part, row0,
+                                      n_total);
+}
+
 constexpr int kSplits16 = 8;
 
 }  // namespace
@@ -477,6 +708,15 @@ void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
   *n_small = small;
 }
 
+// Thin tiles (16 or 32 patches) when the batch in them fills at most one
+// round of the CUs: the call is then one block's K-loop long.  0: the tiles above.
+int conv_fc1_16_thin_tile(int64_t n, int cus) {
+  const int64_t per_round = cus >= kSplits16 ? cus / kSplits16 : 1;   // tiles per round
+  if (n <= 16 * per_round) return 16;
+  if (n <= 32 * per_round) return 32;
+  return 0;
+}
+
 template <bool kFp16, class In>
 hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_total,
                         const uint4* w1p, const uint4* convp, float* part, hipStream_t stream) {
@@ -484,12 +724,20 @@ hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_to
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
+  const int thin = conv_fc1_16_thin_tile(n, cus);
+  if (thin) {
+    const dim3 grid((unsigned)((n + thin - 1) / thin * kSplits16));
+    if (thin == 16)
+      return launch_kernel(conv_fc1_16_thin_kernel<kFp16, kSplits16, 16, In>, grid, dim3(kThreads),
+                           0, stream, patches, n, w1p, convp, part, row0, n_total);
+    return launch_kernel(conv_fc1_16_thin_kernel<kFp16, kSplits16, 32, In>, grid, dim3(kThreads), 0,
+                         stream, patches, n, w1p, convp, part, row0, n_total);
+  }
   int64_t n_big = 0, n_small = 0;
   conv_fc1_16_tiles(n, cus, &n_big, &n_small);
   const dim3 grid((unsigned)((n_big + n_small) * kSplits16));
-  conv_fc1_16_kernel<kFp16, kSplits16, In><<<grid, dim3(kThreads), 0, stream>>>(
-      patches, n, n_big, w1p, convp, part, row0, n_total);
-  return hipGetLastError();
+  return launch_kernel(conv_fc1_16_kernel<kFp16, kSplits16, In>, grid, dim3(kThreads), 0, stream,
+                       patches, n, n_big, w1p, convp, part, row0, n_total);
 }
 
 hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,

@@ -508,9 +508,8 @@ hipError_t launch_conv_fc1_8(const uint16_t* patches, int64_t n, int64_t row0, i
   int64_t n_big = 0, n_small = 0;
   conv_fc1_8_tiles(n, cus, &n_big, &n_small);
   const dim3 grid((unsigned)((n_big + n_small) * kSplits8));
-  conv_fc1_8_kernel<kSplits8><<<grid, dim3(kThreads), 0, stream>>>(patches, n, n_big, w1p, convp,
-                                                                   part, row0, n_total);
-  return hipGetLastError();
+  return launch_kernel(conv_fc1_8_kernel<kSplits8>, grid, dim3(kThreads), 0, stream, patches, n,
+                       n_big, w1p, convp, part, row0, n_total);
 }
 
 }  // namespace pointid

@@ -392,8 +392,8 @@ void conv_fc1_f32_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
 
 hipError_t launch_transpose_w1(const float* w1, float* w1t, hipStream_t stream) {
   static_assert(kFc1In % 32 == 0 && kFc1Out % 32 == 0, "whole 32 x 32 tiles");
-  transpose_w1_kernel<<<dim3(kFc1In / 32, kFc1Out / 32), dim3(256), 0, stream>>>(w1, w1t);
-  return hipGetLastError();
+  return launch_kernel(transpose_w1_kernel, dim3(kFc1In / 32, kFc1Out / 32), dim3(256), 0, stream,
+                       w1, w1t);
 }
 
 hipError_t launch_conv_fc1_f32(const float* patches, int64_t n, int64_t row0, int64_t n_total,
@@ -407,9 +407,8 @@ hipError_t launch_conv_fc1_f32(const float* patches, int64_t n, int64_t row0, in
   int64_t n_big = 0, n_small = 0;
   conv_fc1_f32_tiles(n, cus, &n_big, &n_small);
   const dim3 grid((unsigned)((n_big + n_small) * kSplits));
-  conv_fc1_f32_kernel<<<grid, dim3(kThreads), 0, stream>>>(patches, n, n_big, conv_w, conv_b, w1t,
-                                                          part, row0, n_total);
-  return hipGetLastError();
+  return launch_kernel(conv_fc1_f32_kernel, grid, dim3(kThreads), 0, stream, patches, n, n_big,
+                       conv_w, conv_b, w1t, part, row0, n_total);
 }
 
 }  // namespace pointid

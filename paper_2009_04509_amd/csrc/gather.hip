@@ -269,11 +269,8 @@ hipError_t launch_bin_ticks(const PlaneTable& in, const PlaneTable& out, int tic
   bool vec4 = ticks_per_column % 4 == 0;
   for (int i = 0; i < in.n; ++i)
     vec4 = vec4 && (reinterpret_cast<uintptr_t>(in.p[i].image) & 15) == 0 && in.p[i].n_ticks % 4 == 0;
-  if (vec4)
-    bin_ticks_kernel<true><<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
-  else
-    bin_ticks_kernel<false><<<grid, dim3(256), 0, stream>>>(in, out, ticks_per_column);
-  return hipGetLastError();
+  if (vec4) return launch_kernel(bin_ticks_kernel<true>, grid, dim3(256), 0, stream, in, out, ticks_per_column);
+  return launch_kernel(bin_ticks_kernel<false>, grid, dim3(256), 0, stream, in, out, ticks_per_column);
 }
 
 hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t* out,
@@ -281,13 +278,10 @@ hipError_t launch_patches_to_16(bool fp16, const float* in, int64_t n, uint16_t*
   if (n <= 0) return hipSuccess;
   const int64_t n8 = n * kPatchPix / 8;
   const dim3 grid((unsigned)((n8 + 255) / 256));
-  if (fp16)
-    to_16_kernel<true><<<grid, dim3(256), 0, stream>>>(reinterpret_cast<const float4*>(in), n8,
-                                                      reinterpret_cast<uint4*>(out));
-  else
-    to_16_kernel<false><<<grid, dim3(256), 0, stream>>>(reinterpret_cast<const float4*>(in), n8,
-                                                       reinterpret_cast<uint4*>(out));
-  return hipGetLastError();
+  const float4* src = reinterpret_cast<const float4*>(in);
+  uint4* dst = reinterpret_cast<uint4*>(out);
+  if (fp16) return launch_kernel(to_16_kernel<true>, grid, dim3(256), 0, stream, src, n8, dst);
+  return launch_kernel(to_16_kernel<false>, grid, dim3(256), 0, stream, src, n8, dst);
 }
 
 template <class Src>
@@ -296,12 +290,10 @@ hipError_t launch_gather_src(const PlaneTable& planes, const Src& src, int64_t n
   if (n <= 0) return hipSuccess;
   const dim3 grid((unsigned)((n + kWaves - 1) / kWaves));
   if (out_dtype == POINTID_BF16)
-    gather_kernel<POINTID_BF16, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
-  else if (out_dtype == POINTID_FP16)
-    gather_kernel<POINTID_FP16, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
-  else
-    gather_kernel<POINTID_FP32, Src><<<grid, dim3(256), 0, stream>>>(planes, src, n, out);
-  return hipGetLastError();
+    return launch_kernel(gather_kernel<POINTID_BF16, Src>, grid, dim3(256), 0, stream, planes, src, n, out);
+  if (out_dtype == POINTID_FP16)
+    return launch_kernel(gather_kernel<POINTID_FP16, Src>, grid, dim3(256), 0, stream, planes, src, n, out);
+  return launch_kernel(gather_kernel<POINTID_FP32, Src>, grid, dim3(256), 0, stream, planes, src, n, out);
 }
 
 hipError_t launch_gather(const PlaneTable& planes, const int32_t* hits,

@@ -321,28 +321,25 @@ hipError_t launch_hits_mask(const PlaneTable& planes, const HitSteps& st, float 
           planes.p[i].n_ticks % 4 == 0;
   const dim3 grid((unsigned)((st.workers + kMaskWaves - 1) / kMaskWaves));
   if (vec)
-    hits_mask_kernel<true><<<grid, dim3(64 * kMaskWaves), 0, stream>>>(planes, st, threshold,
-                                                                       mask, counts);
-  else
-    hits_mask_kernel<false><<<grid, dim3(64 * kMaskWaves), 0, stream>>>(planes, st, threshold,
-                                                                        mask, counts);
-  return hipGetLastError();
+    return launch_kernel(hits_mask_kernel<true>, grid, dim3(64 * kMaskWaves), 0, stream, planes, st,
+                         threshold, mask, counts);
+  return launch_kernel(hits_mask_kernel<false>, grid, dim3(64 * kMaskWaves), 0, stream, planes, st,
+                       threshold, mask, counts);
 }
 
 hipError_t launch_hits_scan(const int32_t* counts, int32_t n, int64_t* offsets, int64_t* total,
                             hipStream_t stream) {
   if (n > kHitMaxWorkers) return hipErrorInvalidValue;
-  hits_scan_kernel<<<dim3(1), dim3(kScanThreads), 0, stream>>>(counts, n, offsets, total);
-  return hipGetLastError();
+  return launch_kernel(hits_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, counts, n, offsets,
+                       total);
 }
 
 hipError_t launch_hits_emit(const PlaneTable& planes, const HitSteps& st, const uint64_t* mask,
                             const int32_t* counts, const int64_t* offsets, int32_t* hits,
                             int64_t capacity, hipStream_t stream) {
   if (st.workers <= 0 || capacity <= 0) return hipSuccess;
-  hits_emit_kernel<<<dim3((unsigned)st.workers), dim3(64 * kEmitWaves), 0, stream>>>(planes, st, mask, counts, offsets,
-                                                               hits, capacity);
-  return hipGetLastError();
+  return launch_kernel(hits_emit_kernel, dim3((unsigned)st.workers), dim3(64 * kEmitWaves), 0, stream,
+                       planes, st, mask, counts, offsets, hits, capacity);
 }
 
 }  // namespace pointid

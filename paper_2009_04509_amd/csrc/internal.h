@@ -3,7 +3,10 @@
 #pragma once
 
 #include <string>
+#include <tuple>
+#include <utility>
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "pointid.h"
@@ -11,6 +14,42 @@
 #include <cstdint>
 
 namespace pointid {
+
+// Events the next kernel launched by this thread through launch_kernel
+// attaches to its own dispatch (start: when the kernel begins, stop: when it
+// ends; the library sets only `stop`, a call's completion event, which then
+// needs no packet of its own on the stream).  The next launch takes both (and
+// clears them); a scope that launches nothing leaves them set.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+LaunchEvents& launch_events();    // the calling thread's
+
+// kernel<<<grid, block, shmem, stream>>>(args...), with the calling thread's
+// launch events attached when it has any.  The arguments are converted to the
+// kernel's parameter types before their addresses are taken.
+template <class... KArgs, class... Args>
+hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem,
+                         hipStream_t stream, Args&&... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "argument count");
+  std::tuple<KArgs...> vals(std::forward<Args>(args)...);
+  void* ptrs[sizeof...(KArgs) > 0 ? sizeof...(KArgs) : 1];
+  std::apply([&](auto&... v) {
+    int i = 0;
+    ((ptrs[i++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  LaunchEvents& ev = launch_events();
+  hipError_t e;
+  if (ev.start || ev.stop) {
+    e = hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, shmem, stream,
+                           ev.start, ev.stop, 0);
+    ev = LaunchEvents();
+  } else {
+    e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, shmem, stream);
+  }
+  return e;
+}
 
 constexpr int kPatch = 48;                  // patch side (paper §2.1)
 constexpr int kHalf = 24;                   // hit sits at patch pixel (24, 24)
@@ -126,8 +165,10 @@ int handle_device(pointid_handle h);
 // for s < conv_fc1_16_splits().
 int conv_fc1_16_splits();
 // Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
-// then n_small of 32.
+// then n_small of 32 (a batch that fits one round of thin tiles of 16 or 32
+// patches, conv_fc1_16_thin_tile, runs those instead).
 void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
+int conv_fc1_16_thin_tile(int64_t n, int cus);
 hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);

@@ -105,29 +105,30 @@ __global__ __launch_bounds__(256) void pack_fc1_8_kernel(const float* __restrict
 
 hipError_t launch_pack_conv_fp16(const float* conv_w, const float* conv_b, uint4* conv_frag,
                                  hipStream_t stream) {
-  pack_conv_kernel<true><<<dim3(6), dim3(64), 0, stream>>>(conv_w, conv_b, conv_frag);
-  return hipGetLastError();
+  return launch_kernel(pack_conv_kernel<true>, dim3(6), dim3(64), 0, stream, conv_w, conv_b, conv_frag);
 }
 
 hipError_t launch_pack_fc1_8(const float* fc1_w, const int* exp2, uint8_t* fc1_frag8,
                              hipStream_t stream) {
   const unsigned blocks = (unsigned)(((int64_t)(kPos / 2) * 8 * 64 + 255) / 256);
-  pack_fc1_8_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(fc1_w, exp2, fc1_frag8);
-  return hipGetLastError();
+  return launch_kernel(pack_fc1_8_kernel, dim3(blocks), dim3(256), 0, stream, fc1_w, exp2, fc1_frag8);
 }
 
 hipError_t launch_pack_16(bool fp16, const float* conv_w, const float* conv_b,
                           const float* fc1_w, uint4* conv_frag, uint4* fc1_frag,
                           hipStream_t stream) {
   const unsigned blocks = (unsigned)((kFc1Frags + 255) / 256);
+  hipError_t e;
   if (fp16) {
-    pack_conv_kernel<true><<<dim3(6), dim3(64), 0, stream>>>(conv_w, conv_b, conv_frag);
-    pack_fc1_kernel<true><<<dim3(blocks), dim3(256), 0, stream>>>(fc1_w, fc1_frag);
+    e = launch_kernel(pack_conv_kernel<true>, dim3(6), dim3(64), 0, stream, conv_w, conv_b, conv_frag);
+    if (e == hipSuccess)
+      e = launch_kernel(pack_fc1_kernel<true>, dim3(blocks), dim3(256), 0, stream, fc1_w, fc1_frag);
   } else {
-    pack_conv_kernel<false><<<dim3(6), dim3(64), 0, stream>>>(conv_w, conv_b, conv_frag);
-    pack_fc1_kernel<false><<<dim3(blocks), dim3(256), 0, stream>>>(fc1_w, fc1_frag);
+    e = launch_kernel(pack_conv_kernel<false>, dim3(6), dim3(64), 0, stream, conv_w, conv_b, conv_frag);
+    if (e == hipSuccess)
+      e = launch_kernel(pack_fc1_kernel<false>, dim3(blocks), dim3(256), 0, stream, fc1_w, fc1_frag);
   }
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace pointid

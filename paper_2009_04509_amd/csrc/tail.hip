@@ -188,12 +188,10 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
   if (blocks < kSmallLaunch)
-    tail_kernel<PlainOut, kAllSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        part, splits, n, w, PlainOut{scores});
-  else
-    tail_kernel<PlainOut, kFewSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        part, splits, n, w, PlainOut{scores});
-  return hipGetLastError();
+    return launch_kernel(tail_kernel<PlainOut, kAllSplits>, dim3((unsigned)blocks), dim3(256), 0,
+                         stream, part, splits, n, w, PlainOut{scores});
+  return launch_kernel(tail_kernel<PlainOut, kFewSplits>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       part, splits, n, w, PlainOut{scores});
 }
 
 hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
@@ -204,12 +202,10 @@ hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeigh
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
   if (blocks < kSmallLaunch)
-    tail_kernel<RequestOut, kAllSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        part, splits, n, w, RequestOut{reqs});
-  else
-    tail_kernel<RequestOut, kFewSplits><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-        part, splits, n, w, RequestOut{reqs});
-  return hipGetLastError();
+    return launch_kernel(tail_kernel<RequestOut, kAllSplits>, dim3((unsigned)blocks), dim3(256), 0,
+                         stream, part, splits, n, w, RequestOut{reqs});
+  return launch_kernel(tail_kernel<RequestOut, kFewSplits>, dim3((unsigned)blocks), dim3(256), 0,
+                       stream, part, splits, n, w, RequestOut{reqs});
 }
 
 }  // namespace pointid

@@ -344,15 +344,18 @@ def test_permutation_determinism_duplicates(pid, handles, prec):
 def test_tile_shapes_give_the_same_bits(pid, handles, prec):
     """A patch's scores do not depend on the batch around it.
 
-    4,196 patches run as 32 tiles of 96 patches plus 4 tiles of 32 (16-bit
-    paths), or 64 tiles of 64 plus 4 of 32 (fp32), the small tiles at the end
-    of the batch; the same patches classified in other batches land in other
-    tiles and tile shapes, and must give the same bits."""
+    On a 256-CU device the 16-bit paths run 4,196 patches as 44 tiles of 96;
+    3,073 and 4,000 patches as 32 tiles of 96 and then tiles of 32; up to 512
+    patches in thin tiles of 16 and up to 1,024 in thin tiles of 32.  The fp32
+    path runs 4,196 patches as 64 tiles of 64 plus 4 of 32.  The same patches
+    classified in other batches land in other tiles and tile shapes, and must
+    give the same bits."""
     h = _handle(handles, prec)
     P = synth.config4_patches(4196, seed=2024)
     say(f"tile shapes {prec}")
     full = pid.pointid_classify_patches(h, t(P)).cpu().numpy().view(np.uint32)
-    for lo, hi in [(4096, 4196), (0, 96), (4000, 4196), (1, 2), (4195, 4196), (100, 3173)]:
+    for lo, hi in [(4096, 4196), (0, 96), (4000, 4196), (1, 2), (4195, 4196), (100, 3173),
+                   (0, 4000), (0, 512), (96, 1096), (3000, 3513)]:
         part = pid.pointid_classify_patches(h, t(P[lo:hi])).cpu().numpy().view(np.uint32)
         assert np.array_equal(part, full[lo:hi]), f"patches {lo}:{hi}"
 
