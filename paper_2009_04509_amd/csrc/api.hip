@@ -77,6 +77,16 @@ class DeviceScope {
 };
 
 // ---- optional per-kernel timing (pointid_timing_*)
+//
+// The timed kernels of one call form a chain on its stream: the first carries
+// a start and a stop event on its own dispatch (hipExtLaunchKernel), each
+// later one only a stop event, and a kernel's time runs from the end of the
+// one before it to its own end (the launch gap in between, about 0 with no
+// packet between them, is charged to it).  A stop event on a dispatch adds
+// nothing to the stream; a start event leaves a gap of about 5 us and costs
+// the host 10-20 us, and markers recorded around a launch leave about 7 us.
+// Events are reference counted: a record holds its two, and the chain holds
+// its last stop event until the next kernel has taken it as its start.
 struct TimingRec {
   const char* name;
   hipEvent_t a, b;
@@ -86,43 +96,95 @@ struct Timing {
   std::mutex mu;
   std::vector<TimingRec> pending;
   std::map<std::string, std::pair<double, int64_t>> total;
+  std::map<hipEvent_t, int> refs;
+  // with mu held
+  void hold(hipEvent_t e) { ++refs[e]; }
+  void release(hipEvent_t e) {
+    auto it = refs.find(e);
+    if (it == refs.end() || --it->second > 0) return;
+    refs.erase(it);
+    (void)hipEventDestroy(e);
+  }
 };
 Timing& timing() {
   static Timing t;
   return t;
 }
 
-// Brackets the launch in its scope with events on its stream while timing is
-// enabled.  (Events attached to the dispatch itself, through
-// hipExtLaunchKernel, would drop the two markers, but cost the host about
-// 25 us per launch: the host, not the GPU, then sets the pace of small calls.)
+// The calling thread's chain; a call's workspace opens it (nested workspaces
+// share it).
+struct TimingChain {
+  int depth = 0;
+  hipStream_t stream = nullptr;
+  hipEvent_t last = nullptr;                 // held by the chain
+};
+TimingChain& timing_chain() {
+  static thread_local TimingChain c;
+  return c;
+}
+class ChainScope {
+ public:
+  ChainScope() { ++timing_chain().depth; }
+  ~ChainScope() {
+    TimingChain& c = timing_chain();
+    if (--c.depth > 0 || !c.last) return;
+    std::lock_guard<std::mutex> g(timing().mu);
+    timing().release(c.last);
+    c.last = nullptr;
+  }
+};
+
+// Times the one launch in its scope while timing is enabled.
 class KernelTimer {
  public:
   KernelTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
-    if (!timing().on.load(std::memory_order_relaxed)) return;
-    if (hipEventCreate(&a_) != hipSuccess) return;
-    if (hipEventRecord(a_, s_) != hipSuccess) {
-      (void)hipEventDestroy(a_);
+    Timing& T = timing();
+    if (!T.on.load(std::memory_order_relaxed)) return;
+    if (hipEventCreate(&b_) != hipSuccess) return;
+    TimingChain& c = timing_chain();
+    std::lock_guard<std::mutex> g(T.mu);
+    if (c.depth > 0 && c.last && c.stream == s) {
+      a_ = c.last;                           // the previous kernel's end
+    } else if (hipEventCreate(&a_) == hipSuccess) {
+      own_a_ = true;
+    } else {
+      (void)hipEventDestroy(b_);
       return;
     }
+    T.hold(a_);
+    T.hold(b_);
+    LaunchEvents& ev = launch_events();
+    ev.start = own_a_ ? a_ : nullptr;
+    ev.stop = b_;
     active_ = true;
   }
   ~KernelTimer() {
     if (!active_) return;
-    hipEvent_t b;
-    if (hipEventCreate(&b) != hipSuccess) {
-      (void)hipEventDestroy(a_);
+    LaunchEvents& ev = launch_events();
+    const bool launched = ev.stop == nullptr;   // the launch took the events
+    ev = LaunchEvents();
+    Timing& T = timing();
+    std::lock_guard<std::mutex> g(T.mu);
+    if (!launched) {                         // nothing was launched (an empty call)
+      T.release(a_);
+      T.release(b_);
       return;
     }
-    (void)hipEventRecord(b, s_);
-    std::lock_guard<std::mutex> g(timing().mu);
-    timing().pending.push_back({name_, a_, b});
+    TimingChain& c = timing_chain();
+    if (c.depth > 0) {
+      if (c.last) T.release(c.last);
+      c.last = b_;
+      c.stream = s_;
+      T.hold(b_);
+    }
+    T.pending.push_back({name_, a_, b_});
   }
 
  private:
   const char* name_;
   hipStream_t s_;
-  hipEvent_t a_{};
+  hipEvent_t a_{}, b_{};
+  bool own_a_ = false;
   bool active_ = false;
 };
 
@@ -248,6 +310,7 @@ class Workspace {
     done_ = en.done;
   }
 
+  ChainScope chain_;                           // the call's timed kernels
   ScratchPool* pool_;
   hipStream_t s_;
   bool fixed_ = false;
@@ -475,8 +538,8 @@ int pointid_timing_reset(void) {
   std::lock_guard<std::mutex> g(T.mu);
   for (TimingRec& r : T.pending) {
     (void)hipEventSynchronize(r.b);
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
+    T.release(r.a);
+    T.release(r.b);
   }
   T.pending.clear();
   T.total.clear();
@@ -496,8 +559,10 @@ int pointid_timing_query(const char* kernel, double* total_ms, int64_t* launches
     auto& slot = T.total[r.name];
     slot.first += ms;
     slot.second += 1;
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
+  }
+  for (TimingRec& r : T.pending) {
+    T.release(r.a);
+    T.release(r.b);
   }
   T.pending.clear();
   auto it = T.total.find(kernel);
