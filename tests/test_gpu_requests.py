@@ -240,3 +240,31 @@ def test_trim_frees_idle_scratch(pid):
     torch.cuda.synchronize()
     assert pid.pointid_trim(h, 0) == 0
     h.close()
+
+
+def test_scratch_waits_for_the_call_that_used_it(pid):
+    """A call's scratch buffer goes to another stream only once the call's last
+    kernel has finished: its completion event is attached to that kernel's
+    dispatch.  Two event-sized calls on two streams, enqueued back to back with
+    no host wait between them, must each give the bits they give alone (a
+    completion event that reported done too early would hand the first call's
+    buffer to the second while the first still runs)."""
+    h = pid.pointid_create(weights(), "fp16", 0)
+    planes3, hits3 = synth.config3()
+    imgs = [t(p.image) for p in planes3]
+    h1 = t(hits3)
+    h2 = t(np.ascontiguousarray(hits3[::-1]))
+    ref1 = pid.pointid_classify_planes(h, imgs, h1).cpu().numpy().view(np.uint32)
+    ref2 = pid.pointid_classify_planes(h, imgs, h2).cpu().numpy().view(np.uint32)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for rep in range(3):
+        say(f"two streams, round {rep}")
+        with torch.cuda.stream(sa):
+            a = pid.pointid_classify_planes(h, imgs, h1)
+        with torch.cuda.stream(sb):
+            b = pid.pointid_classify_planes(h, imgs, h2)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.cpu().numpy().view(np.uint32), ref1), f"round {rep}: first stream"
+        assert np.array_equal(b.cpu().numpy().view(np.uint32), ref2), f"round {rep}: second stream"
+    h.close()
