@@ -16,8 +16,12 @@ Prints one JSON line on stdout.  `roofline` describes the kernel that takes the
 most time, timed with HIP events on its own stream inside the timed region;
 `gather_roofline` does the same for the patch gather against HBM bandwidth;
 for the event workload with a 16-bit path, `fp32` gives the same call at the
-paper's precision (fp32), timed in the same run; `cpu_baseline` times the fp64
-CPU oracle on a bounded sample of the same workload on this host's cores.
+paper's precision (fp32), timed in the same run; `board_power` reads the
+socket power and clock (amd-smi) while the event runs back to back;
+`cpu_baseline` times the fp64 CPU oracle on a bounded sample of the same
+workload on this host's cores.  The default warmup (100 calls) is longer than
+the chip's power controller takes to settle under full load (30-40 ms), so the
+timed steps measure the sustained rate.
 """
 
 from __future__ import annotations
@@ -69,8 +73,13 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 100; 20 for --config 5 and --find-hits)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before them (default 100, about 0.14 s of the event: under "
+                         "full load the chip's power controller settles over the first 30-40 ms, "
+                         "during which the 16-bit fused kernel runs 5-15 %% slower; 3 for "
+                         "--config 5 and --find-hits)")
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16", "fp8"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
@@ -106,13 +115,22 @@ def parse():
                          "planes at threshold THR instead of classification")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-h2d", action="store_true", help="skip timing the host-to-device copies")
+    ap.add_argument("--sample-power", type=float, default=4.0, metavar="SECONDS",
+                    help="config 3: read socket power and clock (amd-smi) while the call runs "
+                         "back to back for this long after the timed region; 0 skips it")
     ap.add_argument("--no-fp32-block", action="store_true",
                     help="config 3: skip timing the same call at fp32 (the paper's precision)")
     ap.add_argument("--cpu-sample", type=int, default=24576, help="hits timed on the oracle (about 10 s)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 3 device-to-device copies of MIB MiB (a plain copy kernel of "
                          "known size, to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    light = args.config == 5 or args.find_hits is not None
+    if args.steps is None:
+        args.steps = 20 if light else 100
+    if args.warmup is None:
+        args.warmup = 3 if light else 100
+    return args
 
 
 def source_sha(fname):
@@ -280,6 +298,75 @@ def cpu_baseline(sample, n_sample):
             "paper_context": "paper section 3.1: 213 s of single-process TensorFlow inference "
                              "for about 55,000 patches per event, about 258 patches/s per process "
                              "(other hardware; context only)"}
+
+
+def board_power(args, torch, pid, synth, step, precision):
+    """Socket power and shader clock while the step runs back to back for
+    args.sample_power seconds (a host sync every 8 calls), read with
+    `amd-smi metric -p -c` (read-only) about every 0.1 s; samples of the first
+    second (the ramp) are left out.  Shows whether the chip runs at its power
+    cap or at its top clock under this load."""
+    import shutil
+    import subprocess
+    import threading
+    tool = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
+
+    def read():
+        r = subprocess.run([tool, "metric", "-p", "-c", "-g", "0", "--json"],
+                           capture_output=True, text=True, timeout=20)
+        d = json.loads(r.stdout)
+        g = d["gpu_data"][0] if isinstance(d, dict) else d[0]
+        clks = [v["clk"]["value"] for k, v in g["clock"].items()
+                if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)
+                and isinstance(v["clk"].get("value"), (int, float))]
+        return float(g["power"]["socket_power"]["value"]), (float(np.mean(clks)) if clks else None)
+
+    try:
+        read()
+    except Exception as exc:                       # no tool or no reading on this machine
+        return {"tool": "amd-smi metric -p -c", "error": repr(exc)[:200]}
+    h = pid.pointid_create(synth.he_normal_weights(), precision, 0)
+    for _ in range(3):
+        step(h)
+    torch.cuda.synchronize()
+    stop, samples = threading.Event(), []
+
+    def sampler():
+        while not stop.is_set():
+            t = time.perf_counter()
+            try:
+                samples.append((t,) + read())
+            except Exception:
+                pass
+            time.sleep(0.1)
+
+    th = threading.Thread(target=sampler)
+    t0 = time.perf_counter()
+    th.start()
+    calls = 0
+    while time.perf_counter() - t0 < args.sample_power:
+        for _ in range(8):
+            step(h)
+        calls += 8
+        torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    stop.set()
+    th.join()
+    h.close()
+    kept = [x for x in samples if x[0] - t0 >= 1.0]
+    pw = np.array([x[1] for x in kept])
+    ck = np.array([x[2] for x in kept if x[2] is not None])
+    out = {"tool": "amd-smi metric -p -c (socket power, mean gfx clock over XCDs)",
+           "precision": precision, "seconds": round(dt, 2), "calls": calls,
+           "ms_per_call": round(dt * 1e3 / max(calls, 1), 4), "samples": int(len(kept))}
+    if len(pw):
+        out["socket_power_w"] = {"median": float(np.median(pw)), "min": float(pw.min()), "max": float(pw.max())}
+    if len(ck):
+        out["gfx_clock_mhz"] = {"median": round(float(np.median(ck)), 1), "min": round(float(ck.min()), 1),
+                                "max": round(float(ck.max()), 1)}
+    log(f"[bench] board power over {dt:.1f} s ({calls} calls): {out.get('socket_power_w')} W, "
+        f"clock {out.get('gfx_clock_mhz')} MHz")
+    return out
 
 
 def transfer(args, torch, sample, n):
@@ -675,6 +762,8 @@ def main():
                        "unit": "patches/s", "ms_per_step": round(r32["ms_step"], 4),
                        "step_ms": r32["step_ms"], "roofline": r32["roofline"],
                        "kernels": r32["kernels"]}
+    if args.sample_power > 0 and args.config == 3:
+        out["board_power"] = board_power(args, torch, pid, synth, step, args.precision)
     if not args.no_h2d and args.config in (2, 3):
         out["h2d"] = transfer(args, torch, sample, n)
     if not args.no_cpu_baseline:

@@ -6,9 +6,9 @@
 // size in HBM traffic if written out and read back.  Here the conv is FC1's
 // operand producer: the maps exist only in registers.
 //
-// Work split.  A block owns 96 patches (32 in the blocks that finish a batch:
-// see conv_fc1_16_tiles; small batches run the thin tiles further below, with
-// the same sums) and one of kSplits contiguous ranges of
+// Work split.  A block owns 96 patches (64 in the blocks of the last rounds of
+// some batches: see conv_fc1_16_tiles; small batches run the thin tiles
+// further below, with the same sums) and one of kSplits contiguous ranges of
 // map positions (split-K); blockIdx % 8 selects the range, so every block on one
 // XCD reads the same 1/8 of the FC1 weights and that slice (2.97 MB) stays in
 // the XCD's 4 MB L2.  Positions are taken in pairs (x, x+1) with x even: the
@@ -57,7 +57,7 @@ constexpr int kRing = 8;                      // patch-row ring slots
 constexpr int kPrologueRows = 2 + 5 - 1;
 constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
 constexpr int kBigTile = 96;                  // patches per block (most blocks)
-constexpr int kSmallTile = 32;                // patches per block (the last ones)
+constexpr int kMidTile = 64;                  // patches per block (the last rounds, some batches)
 
 // Layout of a block of kBt patches.  LDS (dwords): ring | conv filter
 // fragments | swap buffers; the final reduction reuses it from the start.
@@ -83,7 +83,7 @@ struct Tile {
   static_assert(kRowMain % 64 == 0 && kRowExtra % 64 == 0 && kRowExtra <= kThreads,
                 "row chunking in whole waves");
 };
-static_assert(Tile<kBigTile>::kLdsDwords >= Tile<kSmallTile>::kLdsDwords, "LDS sized by the big tile");
+static_assert(Tile<kBigTile>::kLdsDwords >= Tile<kMidTile>::kLdsDwords, "LDS sized by the big tile");
 
 // Patches past the end of the batch are read from the last patch instead:
 // their results are never stored.  `In` is the patches' element type: 16-bit
@@ -437,7 +437,7 @@ __device__ __forceinline__ void conv_fc1_block(
   }
 }
 
-// Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A
+// Tiles t < n_big hold kBigTile patches, the ones after them kMidTile.  A
 // patch's sums do not depend on the size of the tile it is in: every MFMA
 // column and every reduction step is per patch.
 template <bool kFp16, int kSplits, class In>
@@ -451,9 +451,9 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
     conv_fc1_block<kFp16, kSplits, kBigTile, In>(lds, split, t * kBigTile, patches, n, w1p, convp,
                                                  part, row0, n_total);
   else
-    conv_fc1_block<kFp16, kSplits, kSmallTile, In>(lds, split,
-                                                   n_big * kBigTile + (t - n_big) * kSmallTile,
-                                                   patches, n, w1p, convp, part, row0, n_total);
+    conv_fc1_block<kFp16, kSplits, kMidTile, In>(lds, split,
+                                                 n_big * kBigTile + (t - n_big) * kMidTile,
+                                                 patches, n, w1p, convp, part, row0, n_total);
 }
 
 
@@ -692,20 +692,38 @@ constexpr int kSplits16 = 8;
 
 int conv_fc1_16_splits() { return kSplits16; }
 
-// One block per CU and (tile, split): the big tiles fill whole rounds of the
-// CUs; what is left (less than one round of big tiles) is cut into small tiles
-// when they fit in one round, which then ends in about half the time.
-void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small) {
+// One block per CU and (tile, split), so a round of the CUs holds `per_round`
+// tiles.  Whole rounds of big tiles, then the rest as rounds of mid tiles or
+// of big tiles, whichever ends first by the relative round time of mid
+// tiles (a 64-patch block takes about 0.72 of a 96-patch block's time: its
+// weight fragments feed 4 MFMAs instead of 6).  Giving up one or two rounds
+// of big tiles for rounds of mid tiles often ends sooner than a last, partly
+// filled round of big tiles (B = 16,384: 4 rounds of 96 and 2 of 64 = 5.44
+// against 6 rounds of 96).  (A last round of 32-patch tiles, at about 0.55 of
+// a big round, never beats two rounds of mid tiles after one big round fewer;
+// batches of at most one round of 32-patch tiles run thin tiles.)
+void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_mid) {
+  constexpr double kRoundMid = 0.72;
   const int64_t per_round = cus >= kSplits16 ? cus / kSplits16 : 1;   // tiles per round
-  int64_t big = n / (kBigTile * per_round) * per_round;
-  const int64_t rest = n - big * kBigTile;
-  int64_t small = (rest + kSmallTile - 1) / kSmallTile;
-  if (small > per_round) {                   // more than one round of small tiles
-    big += (rest + kBigTile - 1) / kBigTile;
-    small = 0;
+  const int64_t full = n / (kBigTile * per_round);
+  auto rounds = [&](int64_t tiles) { return (tiles + per_round - 1) / per_round; };
+  double best = 0.0;
+  bool have = false;
+  for (int64_t r = full; r >= 0 && r >= full - 2; --r) {
+    const int64_t big = r * per_round;
+    const int64_t rest = n - big * kBigTile;
+    const int64_t t_mid = (rest + kMidTile - 1) / kMidTile;
+    const int64_t t_big = (rest + kBigTile - 1) / kBigTile;
+    auto consider = [&](double cost, int64_t b, int64_t m) {
+      if (have && !(cost < best - 1e-9)) return;
+      have = true;
+      best = cost;
+      *n_big = b;
+      *n_mid = m;
+    };
+    consider(r + kRoundMid * (double)rounds(t_mid), big, t_mid);
+    consider(r + (double)rounds(t_big), big + t_big, 0);
   }
-  *n_big = big;
-  *n_small = small;
 }
 
 // Thin tiles (16 or 32 patches) when the batch in them fills at most one
@@ -733,9 +751,9 @@ hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_to
     return launch_kernel(conv_fc1_16_thin_kernel<kFp16, kSplits16, 32, In>, grid, dim3(kThreads), 0,
                          stream, patches, n, w1p, convp, part, row0, n_total);
   }
-  int64_t n_big = 0, n_small = 0;
-  conv_fc1_16_tiles(n, cus, &n_big, &n_small);
-  const dim3 grid((unsigned)((n_big + n_small) * kSplits16));
+  int64_t n_big = 0, n_mid = 0;
+  conv_fc1_16_tiles(n, cus, &n_big, &n_mid);
+  const dim3 grid((unsigned)((n_big + n_mid) * kSplits16));
   return launch_kernel(conv_fc1_16_kernel<kFp16, kSplits16, In>, grid, dim3(kThreads), 0, stream,
                        patches, n, n_big, w1p, convp, part, row0, n_total);
 }

@@ -165,9 +165,9 @@ int handle_device(pointid_handle h);
 // for s < conv_fc1_16_splits().
 int conv_fc1_16_splits();
 // Tiles of the launch over n patches on `cus` CUs: n_big tiles of 96 patches,
-// then n_small of 32 (a batch that fits one round of thin tiles of 16 or 32
+// then n_mid of 64 (a batch that fits one round of thin tiles of 16 or 32
 // patches, conv_fc1_16_thin_tile, runs those instead).
-void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_small);
+void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_mid);
 int conv_fc1_16_thin_tile(int64_t n, int cus);
 hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,

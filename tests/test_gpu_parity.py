@@ -344,8 +344,8 @@ def test_permutation_determinism_duplicates(pid, handles, prec):
 def test_tile_shapes_give_the_same_bits(pid, handles, prec):
     """A patch's scores do not depend on the batch around it.
 
-    On a 256-CU device the 16-bit paths run 4,196 patches as 44 tiles of 96;
-    3,073 and 4,000 patches as 32 tiles of 96 and then tiles of 32; up to 512
+    On a 256-CU device the 16-bit paths run 4,196 patches as 32 tiles of 96
+    and 18 of 64; 3,073 and 4,000 patches as tiles of 64 only; up to 512
     patches in thin tiles of 16 and up to 1,024 in thin tiles of 32.  The fp32
     path runs 4,196 patches as 64 tiles of 64 plus 4 of 32.  The same patches
     classified in other batches land in other tiles and tile shapes, and must
