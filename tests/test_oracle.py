@@ -312,6 +312,27 @@ def test_permutation_duplicate_and_chunk_invariance():
     assert np.array_equal(oracle.classify(p.image, hits, w, chunk=7), base)
 
 
+def test_logits_give_the_softmax_and_their_magnitudes_are_logged():
+    """The class logits the tie diagnostics use are the ones the softmax head
+    turns into scores (paper section 2.2), and their magnitudes are printed:
+    the fp32 path's 1e-4 score bound rests on |logit| staying moderate with
+    these untrained weights (an fp32 error of about 1e-4 relative in FC1 moves
+    a logit of size L by about 1e-4 L)."""
+    p = synth.config2()
+    w = synth.he_normal_weights()
+    hits = p.hits[:48]
+    P = oracle.gather_patches(p.image, hits)
+    z = oracle.logits(P, w)
+    s = oracle.classify_patches(P, w)
+    zz = np.exp(z - z.max(axis=1, keepdims=True))
+    soft = zz / zz.sum(axis=1, keepdims=True)
+    assert np.abs(soft - s[:, :3]).max() < 1e-6
+    a = np.abs(z)
+    print(f"[oracle logits, config 2, 48 hits] max |z| = {a.max():.3g}, median {np.median(a):.3g}, "
+          f"top-2 gap median {np.median(np.diff(np.sort(s[:, :3], axis=1)[:, 1:], axis=1)):.3g}")
+    assert np.isfinite(z).all()
+
+
 def test_planes_match_single_plane():
     a = synth.gen_plane(64, 300, 3, 1, 20, seed=11)
     b = synth.gen_plane(90, 200, 3, 1, 20, seed=12)
