@@ -303,6 +303,14 @@ def cpu_baseline(sample, n_sample):
                              "(other hardware; context only)"}
 
 
+def env_info(torch, pid):
+    """Versions and the device the line was measured on."""
+    props = torch.cuda.get_device_properties(0)
+    return {"device": props.name, "gcn_arch": getattr(props, "gcnArchName", None),
+            "cus": props.multi_processor_count, "hip": torch.version.hip,
+            "torch": torch.__version__, "libpointid": pid.pointid_version()}
+
+
 def board_power(args, torch, pid, synth, step, precision):
     """Socket power and shader clock while the step runs back to back for
     args.sample_power seconds (a host sync every 8 calls), read with
@@ -613,6 +621,7 @@ def serving(args, torch, pid, synth):
     if batcher is not None:
         batcher.close()
     h.close()
+    out["env"] = env_info(torch, pid)
     print(json.dumps(out), flush=True)
 
 
@@ -701,6 +710,7 @@ def hit_finding(args, torch, pid, synth):
         got = out[:min(n_hits, cap)].cpu().numpy()
         out_json["matches_oracle"] = bool(len(ref) == n_hits and np.array_equal(got, ref))
     h.close()
+    out_json["env"] = env_info(torch, pid)
     print(json.dumps(out_json), flush=True)
 
 
@@ -790,6 +800,7 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(sample, args.cpu_sample)
+    out["env"] = env_info(torch, pid)
     print(json.dumps(out), flush=True)
 
 
