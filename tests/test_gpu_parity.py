@@ -360,6 +360,23 @@ def test_tile_shapes_give_the_same_bits(pid, handles, prec):
         assert np.array_equal(part, full[lo:hi]), f"patches {lo}:{hi}"
 
 
+@pytest.mark.parametrize("prec", ["bf16", "fp16"])
+def test_schedule_boundaries_give_the_same_bits(pid, handles, prec):
+    """Batch sizes on both sides of every change of tile schedule on a 256-CU
+    device (thin tiles of 16 up to 512 patches and of 32 up to 1,024, one round
+    of 64-patch tiles up to 2,048, one round of 96 up to 3,072, then rounds of
+    64 or of 96 and 64) give the bits the same patches get in one batch of
+    6,200 (32 tiles of 96 and 49 of 64)."""
+    h = _handle(handles, prec)
+    P = synth.config4_patches(6200, seed=77)
+    say(f"schedule boundaries {prec}")
+    full = pid.pointid_classify_patches(h, t(P)).cpu().numpy().view(np.uint32)
+    for size in (512, 513, 1024, 1025, 2048, 2049, 3072, 3073, 6143, 6144):
+        lo = (size * 7) % (6200 - size + 1)
+        part = pid.pointid_classify_patches(h, t(P[lo:lo + size])).cpu().numpy().view(np.uint32)
+        assert np.array_equal(part, full[lo:lo + size]), f"{size} patches at {lo}"
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_edge_hits_and_zero_bias(pid, handles, prec):
     h = _handle(handles, prec)
