@@ -424,11 +424,12 @@ int pointid_client_close(pointid_client c);
  * launches carries HIP events on its own dispatch (hipExtLaunchKernel), on the
  * stream it runs on (the kernels of pointid_gather[_planes] and
  * pointid_downsample are not timed).  The kernels of one call form a chain:
- * the first is timed from its start to its end, each later one from the end
- * of the kernel before it to its own end (so its time includes the launch
- * gap, a few microseconds).  Timing adds one start event per call (a gap of
- * about 5 us before the first kernel) and turns the call's completion event
- * into a packet of its own (another few microseconds).
+ * the first is timed from an event recorded on the stream just before it,
+ * each later one from the end of the kernel before it, each to its own end
+ * (so a kernel's time includes its launch gap, a few microseconds).  Timing
+ * adds that one recorded event per call (a gap of about 3.5 us before the
+ * first kernel) and turns the call's completion event into a packet of its
+ * own (another few microseconds).
  * pointid_timing_query waits for the recorded events of the kernel named
  * `kernel` ("gather", "conv_fc1_16", "conv_fc1_f32", "tail", ...) and returns the
  * summed elapsed milliseconds and the number of launches since the last

@@ -78,13 +78,14 @@ class DeviceScope {
 
 // ---- optional per-kernel timing (pointid_timing_*)
 //
-// The timed kernels of one call form a chain on its stream: the first carries
-// a start and a stop event on its own dispatch (hipExtLaunchKernel), each
-// later one only a stop event, and a kernel's time runs from the end of the
-// one before it to its own end (the launch gap in between, about 0 with no
-// packet between them, is charged to it).  A stop event on a dispatch adds
-// nothing to the stream; a start event leaves a gap of about 5 us and costs
-// the host 10-20 us, and markers recorded around a launch leave about 7 us.
+// The timed kernels of one call form a chain on its stream: the first is timed
+// from an event recorded on the stream just before it, and every kernel
+// carries a stop event on its own dispatch (hipExtLaunchKernel); a kernel's
+// time runs from the end of the one before it (or that first event) to its
+// own end, the launch gap in between charged to it.  A stop event on a
+// dispatch adds nothing to the stream; a recorded event leaves a gap of about
+// 3.5 us (one per call), and a start event on the dispatch about 5 us and
+// 10-20 us of host time.
 // Events are reference counted: a record holds its two, and the chain holds
 // its last stop event until the next kernel has taken it as its start.
 struct TimingRec {
@@ -145,16 +146,18 @@ class KernelTimer {
     std::lock_guard<std::mutex> g(T.mu);
     if (c.depth > 0 && c.last && c.stream == s) {
       a_ = c.last;                           // the previous kernel's end
-    } else if (hipEventCreate(&a_) == hipSuccess) {
-      own_a_ = true;
-    } else {
+    } else if (hipEventCreate(&a_) != hipSuccess) {
+      (void)hipEventDestroy(b_);
+      return;
+    } else if (hipEventRecord(a_, s) != hipSuccess) {
+      (void)hipEventDestroy(a_);
       (void)hipEventDestroy(b_);
       return;
     }
     T.hold(a_);
     T.hold(b_);
     LaunchEvents& ev = launch_events();
-    ev.start = own_a_ ? a_ : nullptr;
+    ev.start = nullptr;
     ev.stop = b_;
     active_ = true;
   }
@@ -184,7 +187,6 @@ class KernelTimer {
   const char* name_;
   hipStream_t s_;
   hipEvent_t a_{}, b_{};
-  bool own_a_ = false;
   bool active_ = false;
 };
 

@@ -2,7 +2,8 @@
 // h1 = ReLU(b1 + sum of the FC1 partial sums [x 2^-k_n on 8-bit handles]), h2 = ReLU(b2 + h1 W2), then the
 // softmax branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
-// A block of 256 threads handles 32 patches.
+// A block of 256 threads handles 32 patches (8 in a launch that cannot fill
+// the chip, so that each group of 32 lanes evaluates one patch).
 //   1. Each thread owns one float4 column slice of 4 patch rows; it issues the
 //      loads of 4 (or, in a small launch, all 8) splits' partials at once
 //      (coalesced 512 B rows) and adds them in ascending split order, adds b1,
@@ -23,7 +24,8 @@
 namespace pointid {
 namespace {
 
-constexpr int kRows = 32;                   // patches per block
+constexpr int kRows = 32;                   // patches per block (full launches)
+constexpr int kSmallRows = 8;               // patches per block (small launches)
 // splits whose loads are in flight together: 4 when the launch fills the
 // chip (116 VGPRs, 4 waves per SIMD), all 8 for a small launch, where a second
 // round of loads would only add latency
@@ -62,17 +64,18 @@ struct RequestOut {
   }
 };
 
-template <class Out, int kMaxSplits>
+template <class Out, int kMaxSplits, int kBlockRows>
 __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
                                                    int64_t n, DeviceWeights w, Out out) {
-  __shared__ __attribute__((aligned(16))) float H[kRows][kPitch];
+  static_assert(kBlockRows % 8 == 0 && kBlockRows <= 32, "whole rows per thread");
+  __shared__ __attribute__((aligned(16))) float H[kBlockRows][kPitch];
   __shared__ __attribute__((aligned(16))) float W2s[kFc1Out * kFc2Out];
   // output rows, kept as global-address-space pointers so that the stores
   // are global (not flat) stores
-  __shared__ global_float4* dst[kRows];
+  __shared__ global_float4* dst[kBlockRows];
   const int tid = threadIdx.x;
-  const int64_t p0 = (int64_t)blockIdx.x * kRows;
-  if (tid < kRows && p0 + tid < n) dst[tid] = reinterpret_cast<global_float4*>(reinterpret_cast<uintptr_t>(out.row(p0 + tid)));
+  const int64_t p0 = (int64_t)blockIdx.x * kBlockRows;
+  if (tid < kBlockRows && p0 + tid < n) dst[tid] = reinterpret_cast<global_float4*>(reinterpret_cast<uintptr_t>(out.row(p0 + tid)));
   // W2 (16 KiB) into LDS: 4 float4 per thread, coalesced
   for (int i = tid; i < kFc1Out * kFc2Out / 4; i += 256)
     reinterpret_cast<float4*>(W2s)[i] = reinterpret_cast<const float4*>(w.fc2_w)[i];
@@ -81,17 +84,17 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
   {
     const int c4 = tid & 31;                 // float4 column
     const int r0 = tid >> 5;                 // rows r0, r0 + 8, ...
-    float4 acc[kRows / 8];
+    float4 acc[kBlockRows / 8];
 #pragma unroll
-    for (int k = 0; k < kRows / 8; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < kBlockRows / 8; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s0 = 0; s0 < splits; s0 += kMaxSplits) {
-      float4 v[kMaxSplits][kRows / 8];
+      float4 v[kMaxSplits][kBlockRows / 8];
 #pragma unroll
       for (int s = 0; s < kMaxSplits; ++s) {
         const float4* src =
             reinterpret_cast<const float4*>(part + ((int64_t)(s0 + s) * n + p0) * kFc1Out);
 #pragma unroll
-        for (int k = 0; k < kRows / 8; ++k) {
+        for (int k = 0; k < kBlockRows / 8; ++k) {
           const int r = r0 + 8 * k;
           v[s][k] = (s0 + s < splits && p0 + r < n) ? src[r * (kFc1Out / 4) + c4]
                                                      : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -100,17 +103,17 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
 #pragma unroll
       for (int s = 0; s < kMaxSplits; ++s)
 #pragma unroll
-        for (int k = 0; k < kRows / 8; ++k) add4(acc[k], v[s][k]);
+        for (int k = 0; k < kBlockRows / 8; ++k) add4(acc[k], v[s][k]);
     }
     const float4 b = reinterpret_cast<const float4*>(w.fc1_b)[c4];
     if (w.fc1_scale) {                       // 8-bit handles: the sums times 2^-k_n (exact)
       const float4 sc = reinterpret_cast<const float4*>(w.fc1_scale)[c4];
 #pragma unroll
-      for (int k = 0; k < kRows / 8; ++k)
+      for (int k = 0; k < kBlockRows / 8; ++k)
         acc[k] = make_float4(acc[k].x * sc.x, acc[k].y * sc.y, acc[k].z * sc.z, acc[k].w * sc.w);
     }
 #pragma unroll
-    for (int k = 0; k < kRows / 8; ++k) {
+    for (int k = 0; k < kBlockRows / 8; ++k) {
       const int r = r0 + 8 * k;
       *reinterpret_cast<float4*>(&H[r][4 * c4]) =
           make_float4(fmaxf(acc[k].x + b.x, 0.f), fmaxf(acc[k].y + b.y, 0.f),
@@ -146,7 +149,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
     float wc[kFc1Out];
 #pragma unroll
     for (int i = 0; i < kFc1Out; ++i) wc[i] = W2s[i * kFc2Out + j];
-    for (int r = grp; r < kRows; r += 8) {
+    for (int r = grp; r < kBlockRows; r += 8) {
       if (p0 + r >= n) break;
       // the same two half sums, added in the same order, as the full-launch
       // layout: a patch's bits do not depend on the launch it is in
@@ -165,7 +168,7 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
     float wc[kHalfIn];
 #pragma unroll
     for (int i = 0; i < kHalfIn; ++i) wc[i] = W2s[(half * kHalfIn + i) * kFc2Out + j];
-    for (int r = wave; r < kRows; r += 4) {
+    for (int r = wave; r < kBlockRows; r += 4) {
       if (p0 + r >= n) break;
       float hp = 0.f;
 #pragma unroll
@@ -177,7 +180,8 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
   }
 }
 
-// fewer blocks than the chip's CUs: a launch that cannot fill the chip
+// fewer blocks of 32 patches than the chip's CUs: a launch that cannot fill
+// the chip, which then runs blocks of 8 patches
 constexpr int64_t kSmallLaunch = 256;
 
 }  // namespace
@@ -188,10 +192,11 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
   if (blocks < kSmallLaunch)
-    return launch_kernel(tail_kernel<PlainOut, kAllSplits>, dim3((unsigned)blocks), dim3(256), 0,
-                         stream, part, splits, n, w, PlainOut{scores});
-  return launch_kernel(tail_kernel<PlainOut, kFewSplits>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       part, splits, n, w, PlainOut{scores});
+    return launch_kernel(tail_kernel<PlainOut, kAllSplits, kSmallRows>,
+                         dim3((unsigned)((n + kSmallRows - 1) / kSmallRows)), dim3(256), 0, stream,
+                         part, splits, n, w, PlainOut{scores});
+  return launch_kernel(tail_kernel<PlainOut, kFewSplits, kRows>, dim3((unsigned)blocks), dim3(256), 0,
+                       stream, part, splits, n, w, PlainOut{scores});
 }
 
 hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeights& w,
@@ -202,10 +207,11 @@ hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeigh
   if (splits < 1) return hipErrorInvalidValue;
   const int64_t blocks = (n + kRows - 1) / kRows;
   if (blocks < kSmallLaunch)
-    return launch_kernel(tail_kernel<RequestOut, kAllSplits>, dim3((unsigned)blocks), dim3(256), 0,
-                         stream, part, splits, n, w, RequestOut{reqs});
-  return launch_kernel(tail_kernel<RequestOut, kFewSplits>, dim3((unsigned)blocks), dim3(256), 0,
-                       stream, part, splits, n, w, RequestOut{reqs});
+    return launch_kernel(tail_kernel<RequestOut, kAllSplits, kSmallRows>,
+                         dim3((unsigned)((n + kSmallRows - 1) / kSmallRows)), dim3(256), 0, stream,
+                         part, splits, n, w, RequestOut{reqs});
+  return launch_kernel(tail_kernel<RequestOut, kFewSplits, kRows>, dim3((unsigned)blocks), dim3(256),
+                       0, stream, part, splits, n, w, RequestOut{reqs});
 }
 
 }  // namespace pointid
