@@ -316,7 +316,9 @@ def board_power(args, torch, pid, synth, step, precision):
     args.sample_power seconds (a host sync every 8 calls), read with
     `amd-smi metric -p -c` (read-only) about every 0.1 s; samples of the first
     second (the ramp) are left out.  Shows whether the chip runs at its power
-    cap or at its top clock under this load."""
+    cap or at its top clock under this load; the hotspot temperature before
+    and just after the load is context for boxes whose sockets settle at
+    different powers."""
     import shutil
     import subprocess
     import threading
@@ -331,6 +333,19 @@ def board_power(args, torch, pid, synth, step, precision):
                 if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)
                 and isinstance(v["clk"].get("value"), (int, float))]
         return float(g["power"]["socket_power"]["value"]), (float(np.mean(clks)) if clks else None)
+
+    def hotspot():
+        # a separate query: the temperature is only context, so a missing
+        # field costs nothing but this reading
+        try:
+            r = subprocess.run([tool, "metric", "-t", "-g", "0", "--json"],
+                               capture_output=True, text=True, timeout=20)
+            d = json.loads(r.stdout)
+            g = d["gpu_data"][0] if isinstance(d, dict) else d[0]
+            v = g["temperature"]["hotspot"]["value"]
+            return float(v) if isinstance(v, (int, float)) else None
+        except Exception:
+            return None
 
     try:
         read()
@@ -352,6 +367,7 @@ def board_power(args, torch, pid, synth, step, precision):
             time.sleep(0.1)
 
     th = threading.Thread(target=sampler)
+    t_idle = hotspot()
     t0 = time.perf_counter()
     th.start()
     calls = 0
@@ -360,6 +376,7 @@ def board_power(args, torch, pid, synth, step, precision):
             step(h)
         calls += 8
         torch.cuda.synchronize()
+    t_load = hotspot()                             # just after the last calls
     dt = time.perf_counter() - t0
     stop.set()
     th.join()
@@ -367,7 +384,8 @@ def board_power(args, torch, pid, synth, step, precision):
     kept = [x for x in samples if x[0] - t0 >= 1.0]
     pw = np.array([x[1] for x in kept])
     ck = np.array([x[2] for x in kept if x[2] is not None])
-    out = {"tool": "amd-smi metric -p -c (socket power, mean gfx clock over XCDs)",
+    out = {"tool": "amd-smi metric -p -c (socket power, mean gfx clock over XCDs); "
+                   "metric -t (hotspot, before and just after the load)",
            "precision": precision, "seconds": round(dt, 2), "calls": calls,
            "ms_per_call": round(dt * 1e3 / max(calls, 1), 4), "samples": int(len(kept))}
     if len(pw):
@@ -375,6 +393,7 @@ def board_power(args, torch, pid, synth, step, precision):
     if len(ck):
         out["gfx_clock_mhz"] = {"median": round(float(np.median(ck)), 1), "min": round(float(ck.min()), 1),
                                 "max": round(float(ck.max()), 1)}
+    out["hotspot_c"] = {"before": t_idle, "end": t_load}
     log(f"[bench] board power over {dt:.1f} s ({calls} calls): {out.get('socket_power_w')} W, "
         f"clock {out.get('gfx_clock_mhz')} MHz")
     return out
