@@ -2,21 +2,17 @@
 // h1 = ReLU(b1 + sum of the FC1 partial sums [x 2^-k_n on 8-bit handles]), h2 = ReLU(b2 + h1 W2), then the
 // softmax branch (3 outputs) and the sigmoid (Michel) branch (1 output), in fp32.
 //
-// A block of 256 threads handles 32 patches (8 in a launch that cannot fill
-// the chip, so that each group of 32 lanes evaluates one patch).
-//   1. Each thread owns one float4 column slice of 4 patch rows; it issues the
-//      loads of 4 (or, in a small launch, all 8) splits' partials at once
-//      (coalesced 512 B rows) and adds them in ascending split order, adds b1,
-//      applies ReLU and stores h1 in LDS.
-//   2. W2 (16 KB) is staged once per block through LDS into registers.  In a
-//      launch that fills the chip, a wave evaluates one patch at a time: lane
-//      (half, j) keeps rows 64 half .. 64 half + 63 of column j and forms its
-//      half of h2[j] from h1 broadcast out of LDS, the halves added across
-//      lanes j and j + 32 (116 registers with 4 splits in flight, so 4 waves
-//      share a SIMD).  In a small launch a group of 32 lanes evaluates one
-//      patch at a time, lane j keeping all of column j (fewer patches per lane
-//      in sequence: the lower latency).  The four head inputs are reduced
-//      across 32 lanes by a fixed butterfly.
+// A block of 256 threads handles 8 patches, one per group of 32 lanes.
+//   1. Each thread owns one float4 column slice of one patch row; it issues the
+//      loads of all 8 splits' partials at once (coalesced 512 B rows) and adds
+//      them in ascending split order, adds b1, applies ReLU and stores h1 in LDS.
+//   2. W2 (16 KB) is staged once per block through LDS into registers: lane j
+//      of a group keeps column j and forms h2[j] from h1 broadcast out of LDS,
+//      as two half sums (inputs 0-63, then 64-127) added in that order.  The
+//      four head inputs are reduced across the 32 lanes by a fixed butterfly.
+// 80 VGPRs, so 6 waves share a SIMD: 8-patch blocks keep more of the
+// partials' loads in flight than 32-patch blocks with half the splits' loads
+// at once (event, 50,000 patches: 42.3 against 47.5 us).
 // Every patch is computed by the same instruction sequence whatever its
 // position, so results do not depend on the batch or the hit order.
 #include "internal.h"
@@ -24,12 +20,8 @@
 namespace pointid {
 namespace {
 
-constexpr int kRows = 32;                   // patches per block (full launches)
-constexpr int kSmallRows = 8;               // patches per block (small launches)
-// splits whose loads are in flight together: 4 when the launch fills the
-// chip (116 VGPRs, 4 waves per SIMD), all 8 for a small launch, where a second
-// round of loads would only add latency
-constexpr int kFewSplits = 4, kAllSplits = 8;
+constexpr int kRows = 8;                    // patches per block, one per 32 lanes
+constexpr int kSplitsInFlight = 8;          // splits whose loads are issued together
 constexpr int kPitch = kFc1Out + 4;        // LDS row pitch (floats)
 typedef float vec4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) vec4 global_float4;
@@ -64,10 +56,11 @@ struct RequestOut {
   }
 };
 
-template <class Out, int kMaxSplits, int kBlockRows>
+template <class Out>
 __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ part, int splits,
                                                    int64_t n, DeviceWeights w, Out out) {
-  static_assert(kBlockRows % 8 == 0 && kBlockRows <= 32, "whole rows per thread");
+  constexpr int kBlockRows = kRows;
+  constexpr int kMaxSplits = kSplitsInFlight;
   __shared__ __attribute__((aligned(16))) float H[kBlockRows][kPitch];
   __shared__ __attribute__((aligned(16))) float W2s[kFc1Out * kFc2Out];
   // output rows, kept as global-address-space pointers so that the stores
@@ -143,16 +136,14 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
       *dst[r] = (vec4){e0 * inv, e1 * inv, e2 * inv, sig};
     }
   };
-  if constexpr (kMaxSplits == kAllSplits) {
-    // small launch: 8 groups of 32 lanes, lane j holding column j of W2
+  {
+    // 8 groups of 32 lanes, lane j holding column j of W2
     const int grp = tid >> 5;
     float wc[kFc1Out];
 #pragma unroll
     for (int i = 0; i < kFc1Out; ++i) wc[i] = W2s[i * kFc2Out + j];
     for (int r = grp; r < kBlockRows; r += 8) {
       if (p0 + r >= n) break;
-      // the same two half sums, added in the same order, as the full-launch
-      // layout: a patch's bits do not depend on the launch it is in
       float h0 = 0.f, h1 = 0.f;
 #pragma unroll
       for (int i = 0; i < kFc1Out / 2; ++i) h0 = fmaf(H[r][i], wc[i], h0);
@@ -160,29 +151,8 @@ __global__ __launch_bounds__(256) void tail_kernel(const float* __restrict__ par
       for (int i = kFc1Out / 2; i < kFc1Out; ++i) h1 = fmaf(H[r][i], wc[i], h1);
       finish(r, h0 + h1, j == 0);
     }
-  } else {
-    // full launch: a wave per patch, lane (half, j) holding 64 rows of column j
-    const int half = (tid >> 5) & 1;
-    const int wave = tid >> 6;               // 4 waves
-    constexpr int kHalfIn = kFc1Out / 2;
-    float wc[kHalfIn];
-#pragma unroll
-    for (int i = 0; i < kHalfIn; ++i) wc[i] = W2s[(half * kHalfIn + i) * kFc2Out + j];
-    for (int r = wave; r < kBlockRows; r += 4) {
-      if (p0 + r >= n) break;
-      float hp = 0.f;
-#pragma unroll
-      for (int i = 0; i < kHalfIn; ++i) hp = fmaf(H[r][half * kHalfIn + i], wc[i], hp);
-      // both halves form (inputs 0-63) + (inputs 64-127)
-      const float ho = __shfl_xor(hp, 32);
-      finish(r, half == 0 ? hp + ho : ho + hp, tid % 64 == 0);
-    }
   }
 }
-
-// fewer blocks of 32 patches than the chip's CUs: a launch that cannot fill
-// the chip, which then runs blocks of 8 patches
-constexpr int64_t kSmallLaunch = 256;
 
 }  // namespace
 
@@ -190,12 +160,7 @@ hipError_t launch_tail(const float* part, int splits, int64_t n, const DeviceWei
                        float* scores, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   if (splits < 1) return hipErrorInvalidValue;
-  const int64_t blocks = (n + kRows - 1) / kRows;
-  if (blocks < kSmallLaunch)
-    return launch_kernel(tail_kernel<PlainOut, kAllSplits, kSmallRows>,
-                         dim3((unsigned)((n + kSmallRows - 1) / kSmallRows)), dim3(256), 0, stream,
-                         part, splits, n, w, PlainOut{scores});
-  return launch_kernel(tail_kernel<PlainOut, kFewSplits, kRows>, dim3((unsigned)blocks), dim3(256), 0,
+  return launch_kernel(tail_kernel<PlainOut>, dim3((unsigned)((n + kRows - 1) / kRows)), dim3(256), 0,
                        stream, part, splits, n, w, PlainOut{scores});
 }
 
@@ -205,13 +170,8 @@ hipError_t launch_tail_requests(const float* part, int splits, const DeviceWeigh
   const int64_t n = reqs.start[reqs.n];
   if (n <= 0) return hipSuccess;
   if (splits < 1) return hipErrorInvalidValue;
-  const int64_t blocks = (n + kRows - 1) / kRows;
-  if (blocks < kSmallLaunch)
-    return launch_kernel(tail_kernel<RequestOut, kAllSplits, kSmallRows>,
-                         dim3((unsigned)((n + kSmallRows - 1) / kSmallRows)), dim3(256), 0, stream,
-                         part, splits, n, w, RequestOut{reqs});
-  return launch_kernel(tail_kernel<RequestOut, kFewSplits, kRows>, dim3((unsigned)blocks), dim3(256),
-                       0, stream, part, splits, n, w, RequestOut{reqs});
+  return launch_kernel(tail_kernel<RequestOut>, dim3((unsigned)((n + kRows - 1) / kRows)), dim3(256), 0,
+                       stream, part, splits, n, w, RequestOut{reqs});
 }
 
 }  // namespace pointid
