@@ -59,16 +59,6 @@ constexpr int kRP = 26;                       // LDS row pitch, dwords (24 used)
 constexpr int kBigTile = 96;                  // patches per block (most blocks)
 constexpr int kMidTile = 64;                  // patches per block (the last rounds, some batches)
 
-// f(std::integral_constant<int, I>) for I = 0 .. N-1, unrolled
-template <class F, int... I>
-__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_seq(f, std::make_integer_sequence<int, N>{});
-}
-
 // Layout of a block of kBt patches.  LDS (dwords): ring | conv filter
 // fragments | swap buffers; the final reduction reuses it from the start.
 // A patch row (96 B) of each of the block's patches is kBt x 6 chunks of 16 B:
@@ -477,11 +467,12 @@ template <int kBt>
 struct Thin {
   static constexpr int kTiles = kBt / 16;
   static constexpr int kSlot = kBt * kRP;                  // dwords per staged row
-  static constexpr int kRegion = kMT * kTiles * 4 * 64;    // one wave's partial sums
+  // the reduction: per output half, 3 tiles from the other groups per accumulator tile
+  static constexpr int kRed = kNHalves * kMT * kTiles * (kKGroups - 1) * 4 * 64;
   // one row slot more than a range needs: the loop reads the window of the
   // pair after its last one (the result is never used), which may lie one row lower
   static constexpr int kRowsDw = (kThinRows + 1) * kSlot;
-  static constexpr int kLdsDwords = kRowsDw > 4 * kRegion ? kRowsDw : 4 * kRegion;
+  static constexpr int kLdsDwords = kRowsDw > kRed ? kRowsDw : kRed;
   static constexpr int kRowChunks = kBt * 6;               // 16 B chunks per staged row
   static constexpr int kPer = (kThinRows * kRowChunks + kThreads - 1) / kThreads;
   static_assert(kTiles >= 1 && kTiles <= 2, "1 or 2 patch tiles");
@@ -505,7 +496,7 @@ __device__ __forceinline__ void thin_block(
     const uint4* __restrict__ w1p, const uint4* __restrict__ convp, float* __restrict__ part,
     int64_t row0, int64_t n_total) {
   using T = Thin<kBt>;
-  constexpr int kTiles = T::kTiles, kSlot = T::kSlot, kRegion = T::kRegion;
+  constexpr int kTiles = T::kTiles, kSlot = T::kSlot;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -637,44 +628,40 @@ __device__ __forceinline__ void thin_block(
     }
   }
 
-  // ---- the fixed-order reduction of the tiles above: (g0 + g2) + (g1 + g3)
+  // ---- the fixed-order reduction of the tiles above: (g0 + g2) + (g1 + g3),
+  // each position group finishing a quarter of its output half's tiles, as in
+  // the tiles above
   __syncthreads();                           // every wave is done with the rows
+  constexpr int kSlots = kMT * kTiles;
+  constexpr int kPer = kSlots / kKGroups;
+  static_assert(kSlots % kKGroups == 0, "whole quarters");
   floatx4* red = reinterpret_cast<floatx4*>(lds);
-  auto slot = [&](int region, int m, int i) {
-    return region * (kRegion / 4) + (m * kTiles + i) * 64 + lane;
+  auto entry = [&](int q, int src) { return ((nh * kSlots + q) * (kKGroups - 1) + src) * 64 + lane; };
+  auto tile = [&](auto qc) -> floatx4& {
+    constexpr int q = decltype(qc)::value;
+    return acc[q / kTiles][q % kTiles];
   };
-  auto put = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int i = 0; i < kTiles; ++i) red[slot(region, m, i)] = acc[m][i];
-  };
-  auto add = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int i = 0; i < kTiles; ++i) acc[m][i] += red[slot(region, m, i)];
-  };
-  if (kg >= 2) put(nh * 2 + (kg - 2));
+  static_for<kSlots>([&](auto qc) {
+    constexpr int o = decltype(qc)::value / kPer;
+    if (kg != o) red[entry(decltype(qc)::value, kg - (kg > o ? 1 : 0))] = tile(qc);
+  });
   __syncthreads();
-  if (kg < 2) add(nh * 2 + kg);
-  __syncthreads();
-  if (kg == 1) put(nh);
-  __syncthreads();
-  if (kg != 0) return;
-  add(nh);
 
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
+  static_for<kSlots>([&](auto qc) {
+    constexpr int q = decltype(qc)::value, o = q / kPer, m = q / kTiles, i = q % kTiles;
+    if (kg == o) {
+      floatx4 v[kKGroups];
 #pragma unroll
-  for (int i = 0; i < kTiles; ++i) {
-    const int64_t po = (int64_t)i * 16 + col;
-#pragma unroll
-    for (int m = 0; m < kMT; ++m) {
-      const int o = 16 * (nh * kMT + m) + 4 * grp;
+      for (int g = 0; g < kKGroups; ++g)
+        v[g] = (g == o) ? tile(qc) : red[entry(q, g - (g > o ? 1 : 0))];
+      const floatx4 sum = (v[0] + v[2]) + (v[1] + v[3]);
+      const int64_t po = (int64_t)i * 16 + col;
+      const int out = 16 * (nh * kMT + m) + 4 * grp;
       if (p_base + po < n)
-        __builtin_nontemporal_store(acc[m][i], reinterpret_cast<floatx4*>(dst + po * kFc1Out + o));
+        __builtin_nontemporal_store(sum, reinterpret_cast<floatx4*>(dst + po * kFc1Out + out));
     }
-  }
+  });
 }
 
 template <bool kFp16, int kSplits, int kBt, class In>

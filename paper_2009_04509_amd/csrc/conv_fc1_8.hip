@@ -66,9 +66,10 @@ struct Tile8 {
   static constexpr int kSwapOff = kConvOff + 6 * 64 * 4;
   static constexpr int kSwapWave = kOwn * kSwapTile;
   static constexpr int kSwapBuf = kWaves * kSwapWave;
-  static constexpr int kRegion = kMT * kTiles * 4 * 64;
+  // the reduction: per output half, 3 tiles from the other groups per accumulator tile
+  static constexpr int kRed = kNHalves * kMT * kTiles * (kKGroups - 1) * 4 * 64;
   static constexpr int kMain = kSwapOff + 2 * kSwapBuf;
-  static constexpr int kLdsDwords = (kMain > 4 * kRegion) ? kMain : 4 * kRegion;
+  static constexpr int kLdsDwords = (kMain > kRed) ? kMain : kRed;
   static constexpr int kRowChunks = kBt * 6;
   static constexpr int kRowMain = kRowChunks < kThreads ? kRowChunks : kThreads;
   static constexpr int kRowExtra = kRowChunks - kRowMain;
@@ -142,7 +143,7 @@ __device__ __forceinline__ void conv_fc1_8_block(
     const uint8_t* __restrict__ w1p, const uint4* __restrict__ convp, float* __restrict__ part,
     int64_t row0, int64_t n_total) {
   using T = Tile8<kBt>;
-  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot, kRegion = T::kRegion;
+  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot;
   using Op = Op16<true>;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -413,51 +414,43 @@ __device__ __forceinline__ void conv_fc1_8_block(
   if (step < steps) step_fn(step, own_a, own_b);
 
   // ---- fixed-order reduction over position groups, per output half:
-  //      (g0 + g2) + (g1 + g3)
+  //      (g0 + g2) + (g1 + g3), finished by one wave per accumulator tile.
+  // The four waves of an output half hold the same tiles; position group g
+  // finishes the g-th quarter of them, so after one barrier every wave adds
+  // and stores its own quarter.
+  constexpr int kSlots = kMT * kTiles;
+  constexpr int kPer = kSlots / kKGroups;
+  static_assert(kSlots % kKGroups == 0, "whole quarters");
   floatx4* red = reinterpret_cast<floatx4*>(lds);
-  auto slot = [&](int region, int m, int i) {
-    return region * (kRegion / 4) + (m * kTiles + i) * 64 + lane;
+  auto entry = [&](int q, int src) { return ((nh * kSlots + q) * (kKGroups - 1) + src) * 64 + lane; };
+  auto tile = [&](auto qc) -> floatx4& {
+    constexpr int q = decltype(qc)::value, m = q / kTiles, j = q % kTiles;
+    if constexpr (j < kOwn) return acc_own[m][j];
+    else return acc_oth[m][j - kOwn];
   };
-  auto put_acc = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int i = 0; i < kOwn; ++i) {
-        red[slot(region, m, i)] = acc_own[m][i];
-        red[slot(region, m, kOwn + i)] = acc_oth[m][i];
-      }
-  };
-  auto add_acc = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int i = 0; i < kOwn; ++i) {
-        acc_own[m][i] += red[slot(region, m, i)];
-        acc_oth[m][i] += red[slot(region, m, kOwn + i)];
-      }
-  };
-  if (kg >= 2) put_acc(nh * 2 + (kg - 2));
+  static_for<kSlots>([&](auto qc) {
+    constexpr int o = decltype(qc)::value / kPer;
+    if (kg != o) red[entry(decltype(qc)::value, kg - (kg > o ? 1 : 0))] = tile(qc);
+  });
   __syncthreads();
-  if (kg < 2) add_acc(nh * 2 + kg);
-  __syncthreads();
-  if (kg == 1) put_acc(nh);
-  __syncthreads();
-  if (kg != 0) return;
-  add_acc(nh);
 
-  // acc_*[m][i]: outputs 16(nh*kMT + m) + 4*grp + e for patch 16*tile + col
+  // tile q = m * kTiles + j: outputs 16(nh*kMT + m) + 4*grp + e for patch
+  // 16*(block tile) + col, the block tile nh*kOwn + j (own) or
+  // (1-nh)*kOwn + j - kOwn (partner's)
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
+  static_for<kSlots>([&](auto qc) {
+    constexpr int q = decltype(qc)::value, o = q / kPer, m = q / kTiles, j = q % kTiles;
+    if (kg == o) {
+      floatx4 v[kKGroups];
 #pragma unroll
-  for (int i = 0; i < kOwn; ++i) {
-    const int64_t po = (int64_t)(nh * kOwn + i) * 16 + col;
-    const int64_t pp = (int64_t)((1 - nh) * kOwn + i) * 16 + col;
-#pragma unroll
-    for (int m = 0; m < kMT; ++m) {
-      const int o = 16 * (nh * kMT + m) + 4 * grp;
-      if (p_base + po < n) __builtin_nontemporal_store(acc_own[m][i], reinterpret_cast<floatx4*>(dst + po * kFc1Out + o));
-      if (p_base + pp < n) __builtin_nontemporal_store(acc_oth[m][i], reinterpret_cast<floatx4*>(dst + pp * kFc1Out + o));
+      for (int g = 0; g < kKGroups; ++g)
+        v[g] = (g == o) ? tile(qc) : red[entry(q, g - (g > o ? 1 : 0))];
+      const floatx4 sum = (v[0] + v[2]) + (v[1] + v[3]);
+      const int64_t pt = (int64_t)((j < kOwn) ? nh * kOwn + j : (1 - nh) * kOwn + (j - kOwn)) * 16 + col;
+      const int out = 16 * (nh * kMT + m) + 4 * grp;
+      if (p_base + pt < n) __builtin_nontemporal_store(sum, reinterpret_cast<floatx4*>(dst + pt * kFc1Out + out));
     }
-  }
+  });
 }
 
 // Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A

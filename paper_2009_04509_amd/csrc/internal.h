@@ -15,6 +15,16 @@
 
 namespace pointid {
 
+// f(std::integral_constant<int, I>) for I = 0 .. N-1, unrolled
+template <class F, int... I>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
 // Events the next kernel launched by this thread through launch_kernel
 // attaches to its own dispatch (start: when the kernel begins, stop: when it
 // ends; the library sets only `stop`, a call's completion event, which then
