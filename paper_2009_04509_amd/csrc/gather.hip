@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
   constexpr int kPerRow = kPatch / kPix;                 // chunks per patch row
   constexpr int kChunks = kPatch * kPerRow;              // chunks per patch
   constexpr int kIter = (kChunks + 63) / 64;
-  constexpr int kWords = kPix / 4 + 1;                   // aligned words covering a chunk
+  constexpr int kLoads = kPix / 4;                       // 16-byte loads of a chunk
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int64_t i = xcd_major_block(blockIdx.x, gridDim.x) * kWaves + wave;
@@ -130,9 +130,11 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
   if (small) {
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void*>(base), (short)0, (int)span, 0x00020000);
-    // every load of the wave first (all in flight together), then the shifts
-    floatx4 q[kIter][kWords];
-    int mm[kIter];
+    // every load of the wave first (all in flight together): a chunk's
+    // pixels are kPix consecutive floats at a 4-byte aligned offset, read as
+    // kPix / 4 16-byte loads at that offset when they lie inside the image
+    floatx4 q[kIter][kLoads];
+    bool inside[kIter];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
       const int k = lane + 64 * it;
@@ -140,14 +142,13 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
       const int64_t wire = (int64_t)w - kHalf + r;
       const int64_t tick0 = (int64_t)t - kHalf + kPix * hc;
       const bool row_ok = k < kChunks && wire >= 0 && wire < W;
-      // byte offset of the chunk's first pixel from `base`; the words are read
-      // from the 16-byte boundary below it, `m` floats earlier
+      // byte offset of the chunk's first pixel from `base`
       const int64_t rel = (int64_t)lead + 4 * (wire * T + tick0);
-      mm[it] = (int)((rel >> 2) & 3);
+      inside[it] = row_ok && rel >= 0 && rel + 4 * kPix <= (int64_t)span;
       // offsets are taken mod 2^32: every offset at or past 2^31 is out of range
-      const uint32_t a0 = row_ok ? (uint32_t)(rel - 4 * mm[it]) : 0x80000000u;
+      const uint32_t a0 = inside[it] ? (uint32_t)rel : 0x80000000u;
 #pragma unroll
-      for (int j = 0; j < kWords; ++j)
+      for (int j = 0; j < kLoads; ++j)
         q[it][j] = __builtin_bit_cast(
             floatx4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, a0 + 16u * j, 0, 0));
     }
@@ -159,25 +160,17 @@ __global__ __launch_bounds__(256) void gather_kernel(PlaneTable planes, Src src,
       const int64_t wire = (int64_t)w - kHalf + r;
       const int64_t tick0 = (int64_t)t - kHalf + kPix * hc;
       const bool row_ok = k < kChunks && wire >= 0 && wire < W;
-      const int m = mm[it];
-      // pixel j of the chunk is word float m + j: two levels of dword selects
-      // (v_perm_b32 byte selects, which the compiler keeps as value operations)
-      const uint32_t sel1 = (m & 1) ? 0x07060504u : 0x03020100u;
-      const uint32_t sel2 = (m & 2) ? 0x07060504u : 0x03020100u;
-      uint32_t s1[kPix + 2];
-#pragma unroll
-      for (int j = 0; j < kPix + 2; ++j)
-        s1[j] = __builtin_amdgcn_perm(__float_as_uint(q[it][(j + 1) / 4][(j + 1) % 4]),
-                                      __float_as_uint(q[it][j / 4][j % 4]), sel1);
       // columns j_lo <= j < j_hi of the chunk are inside the row
       const int64_t lo64 = -tick0, hi64 = T - tick0;
       const int j_lo = row_ok ? (int)(lo64 < 0 ? 0 : (lo64 > kPix ? kPix : lo64)) : kPix;
       const int j_hi = (int)(hi64 < 0 ? 0 : (hi64 > kPix ? kPix : hi64));
       float v[kPix];
 #pragma unroll
-      for (int j = 0; j < kPix; ++j) {
-        const uint32_t x = __builtin_amdgcn_perm(s1[j + 2], s1[j], sel2);
-        v[j] = (j >= j_lo && j < j_hi) ? __uint_as_float(x) : 0.f;
+      for (int j = 0; j < kPix; ++j) v[j] = (j >= j_lo && j < j_hi) ? q[it][j / 4][j % 4] : 0.f;
+      if (row_ok && !inside[it]) {
+        // a chunk over the first or last bytes of the image: pixel by pixel
+#pragma unroll
+        for (int j = 0; j < kPix; ++j) v[j] = (j >= j_lo && j < j_hi) ? img[wire * T + tick0 + j] : 0.f;
       }
       emit(k, v);
     }
