@@ -30,9 +30,10 @@
 // LDS (dwords): ring of 8 patch rows (patches x 52) | conv filter fragments
 // [6 conv tiles][64 lanes][8] | swap buffers [2][8 waves][own tiles][64 lanes]
 // x 4; the final reduction reuses it from the start.  The four position
-// groups' partial sums are added in a fixed order ((g0 + g2) + (g1 + g3)) and
-// written as fp32 partials [split][patch][128] for the tail kernel: results do
-// not depend on the batch or the hit order.
+// groups' partial sums are added in a fixed order ((g0 + g2) + (g1 + g3)), each
+// group finishing a quarter of the tiles, and written as fp32 partials
+// [split][patch][128] for the tail kernel: results do not depend on the batch
+// or the hit order.
 #include "internal.h"
 
 namespace pointid {
@@ -70,8 +71,9 @@ struct Tile {
   static constexpr int kSwapOff = kFiltOff + kQ * 64 * 8;
   static constexpr int kSwapBuf = kWaves * kOwn * 64 * 4;
   static constexpr int kMain = kSwapOff + 2 * kSwapBuf;
-  static constexpr int kRegion = kMT * kTiles * 64 * 4;   // one wave's partial sums
-  static constexpr int kLds = kMain > 4 * kRegion ? kMain : 4 * kRegion;
+  // the reduction: per output half, 3 tiles from the other groups per accumulator tile
+  static constexpr int kRed = kHalves * kMT * kTiles * (kGroups - 1) * 64 * 4;
+  static constexpr int kLds = kMain > kRed ? kMain : kRed;
   static constexpr int kRowChunks = kBt * 12;
   static constexpr int kRowMain = kRowChunks < kThreads ? kRowChunks : kThreads;
   static constexpr int kRowExtra = kRowChunks - kRowMain;
@@ -112,7 +114,7 @@ __device__ __forceinline__ void conv_fc1_f32_block(
     const float* __restrict__ conv_w, const float* __restrict__ conv_b,
     const float* __restrict__ w1t, float* __restrict__ part, int64_t row0, int64_t n_total) {
   using T = Tile<kBt>;
-  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot, kRegion = T::kRegion;
+  constexpr int kTiles = T::kTiles, kOwn = T::kOwn, kSlot = T::kSlot;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -298,45 +300,42 @@ __device__ __forceinline__ void conv_fc1_f32_block(
     }
   }
 
-  // ---- fixed-order reduction over the position groups: (g0 + g2) + (g1 + g3)
+  // ---- fixed-order reduction over the position groups: (g0 + g2) + (g1 + g3),
+  // each position group finishing a quarter of its output half's accumulator
+  // tiles after one barrier (the four waves of a half hold the same tiles)
+  constexpr int kSlots = kMT * kTiles;
+  constexpr int kPer = kSlots / kGroups;
+  static_assert(kSlots % kGroups == 0, "whole quarters");
   floatx4* red = reinterpret_cast<floatx4*>(lds);
-  auto slot = [&](int region, int m, int j) {
-    return region * (kRegion / 4) + (m * kTiles + j) * 64 + lane;
+  auto entry = [&](int q, int src) { return ((nh * kSlots + q) * (kGroups - 1) + src) * 64 + lane; };
+  auto tile_acc = [&](auto qc) -> floatx4& {
+    constexpr int q = decltype(qc)::value;
+    return acc[q / kTiles][q % kTiles];
   };
-  auto putr = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int j = 0; j < kTiles; ++j) red[slot(region, m, j)] = acc[m][j];
-  };
-  auto addr = [&](int region) {
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-#pragma unroll
-      for (int j = 0; j < kTiles; ++j) acc[m][j] += red[slot(region, m, j)];
-  };
-  if (kg >= 2) putr(nh * 2 + (kg - 2));
+  static_for<kSlots>([&](auto qc) {
+    constexpr int o = decltype(qc)::value / kPer;
+    if (kg != o) red[entry(decltype(qc)::value, kg - (kg > o ? 1 : 0))] = tile_acc(qc);
+  });
   __syncthreads();
-  if (kg < 2) addr(nh * 2 + kg);
-  __syncthreads();
-  if (kg == 1) putr(nh);
-  __syncthreads();
-  if (kg != 0) return;
-  addr(nh);
 
   // acc[m][j]: outputs 16 (nh kMT + m) + 4 grp + e of patch 16 tile + col, tile
   // = nh kOwn + j for j < kOwn, else (1 - nh) kOwn + j - kOwn
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
+  static_for<kSlots>([&](auto qc) {
+    constexpr int q = decltype(qc)::value, o = q / kPer, m = q / kTiles, j = q % kTiles;
+    if (kg == o) {
+      floatx4 v[kGroups];
 #pragma unroll
-  for (int j = 0; j < kTiles; ++j) {
-    const int tile = j < kOwn ? nh * kOwn + j : (1 - nh) * kOwn + (j - kOwn);
-    const int64_t p = (int64_t)tile * 16 + col;
-    if (p_base + p >= n) continue;
-#pragma unroll
-    for (int m = 0; m < kMT; ++m)
-      __builtin_nontemporal_store(acc[m][j], reinterpret_cast<floatx4*>(
-                                                 dst + p * kFc1Out + 16 * (nh * kMT + m) + 4 * grp));
-  }
+      for (int g = 0; g < kGroups; ++g)
+        v[g] = (g == o) ? tile_acc(qc) : red[entry(q, g - (g > o ? 1 : 0))];
+      const floatx4 sum = (v[0] + v[2]) + (v[1] + v[3]);
+      const int tile = j < kOwn ? nh * kOwn + j : (1 - nh) * kOwn + (j - kOwn);
+      const int64_t p = (int64_t)tile * 16 + col;
+      if (p_base + p < n)
+        __builtin_nontemporal_store(sum, reinterpret_cast<floatx4*>(
+                                             dst + p * kFc1Out + 16 * (nh * kMT + m) + 4 * grp));
+    }
+  });
 }
 
 // Tiles t < n_big hold kBigTile patches; the ones after them kSmallTile.  A
