@@ -184,12 +184,27 @@ def test_gather_edges_and_odd_pitch(pid):
 
 
 def test_gather_unaligned_image_base(pid):
+    """Planes whose base is 4, 8 or 12 bytes past a 16-byte boundary: a
+    chunk's pixels are read at their own 4-byte aligned offset, and the
+    chunks over the image's first and last bytes (hits near the first and
+    last wire) pixel by pixel; every output precision must match the oracle
+    bit for bit."""
     img = synth.coord_image(40, 64)
-    buf = t(np.concatenate([[0.0], img.ravel()]).astype(np.float32))
-    view = buf[1:].view(40, 64)                    # base 4 bytes past a 16-byte boundary
-    hits = np.array([[0, 0], [20, 30], [39, 63], [10, 40]], np.int32)
-    got = pid.pointid_gather(view, t(hits), "fp32").cpu().numpy()
-    assert np.array_equal(got, oracle.gather_patches(img, hits))
+    rng = np.random.default_rng(41)
+    hits = np.concatenate([
+        np.array([[0, 0], [20, 30], [39, 63], [10, 40], [0, 63], [39, 0], [1, 2], [38, 61]]),
+        np.stack([rng.integers(-5, 45, 60), rng.integers(-5, 69, 60)], 1),
+    ]).astype(np.int32)
+    ref = oracle.gather_patches(img, hits)
+    for lead in (1, 2, 3):
+        buf = t(np.concatenate([np.zeros(lead), img.ravel()]).astype(np.float32))
+        view = buf[lead:].view(40, 64)             # base 4 * lead bytes past a 16-byte boundary
+        say(f"gather unaligned base, {4 * lead} bytes")
+        got = pid.pointid_gather(view, t(hits), "fp32").cpu().numpy()
+        assert np.array_equal(got, ref)
+        for dt in ("bf16", "fp16"):
+            gotb = pid.pointid_gather(view, t(hits), dt).cpu().numpy()
+            assert np.array_equal(gotb.view(np.uint16), _bits16(ref, dt)), (lead, dt)
 
 
 def test_gather_plane_over_2gib(pid):
