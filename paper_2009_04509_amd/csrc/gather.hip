@@ -218,32 +218,47 @@ __global__ __launch_bounds__(256) void bin_ticks_kernel(PlaneTable in, PlaneTabl
   const int p = blockIdx.z;
   const int64_t T = in.p[p].n_ticks;
   const int64_t J = out.p[p].n_ticks;
+  const int64_t W = in.p[p].n_wires;
   const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (j >= J) return;
   const int n = (int)(T - j * D < D ? T - j * D : D);
   float* o = const_cast<float*>(out.p[p].image);
-  for (int64_t w = blockIdx.y; w < in.p[p].n_wires; w += gridDim.y) {
-    const float* x = in.p[p].image + w * T + j * D;
-    // the loads of 8 ticks at a time are in flight together; the sum still
-    // runs in tick order from the first tick
-    double s = 0.0;
+  // kWires wires per pass, their loads in flight together (4 with float4
+  // loads: 63 against 72 us on the event at D = 4; the scalar loads of other
+  // D keep one wire per pass, where four measured slower); each column's sum
+  // still runs in tick order from its first tick
+  constexpr int kWires = kVec4 ? 4 : 1;
+  const int64_t step = gridDim.y;
+  for (int64_t w0 = blockIdx.y; w0 < W; w0 += kWires * step) {
+    double s[kWires];
     for (int k0 = 0; k0 < n; k0 += 8) {
-      float xs[8];
-      if constexpr (kVec4) {              // n is a multiple of 4 here (T % 4 == 0)
-        const float4* x4 = reinterpret_cast<const float4*>(x + k0);
-        const float4 a = x4[0];
-        const float4 b = k0 + 4 < n ? x4[1] : make_float4(0.f, 0.f, 0.f, 0.f);
-        xs[0] = a.x; xs[1] = a.y; xs[2] = a.z; xs[3] = a.w;
-        xs[4] = b.x; xs[5] = b.y; xs[6] = b.z; xs[7] = b.w;
-      } else {
+      float xs[kWires][8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) xs[k] = k0 + k < n ? x[k0 + k] : 0.f;
+      for (int g = 0; g < kWires; ++g) {
+        const int64_t w = w0 + g * step;
+        const float* x = in.p[p].image + (w < W ? w : W - 1) * T + j * D;
+        if constexpr (kVec4) {              // n is a multiple of 4 here (T % 4 == 0)
+          const float4* x4 = reinterpret_cast<const float4*>(x + k0);
+          const float4 a = x4[0];
+          const float4 b = k0 + 4 < n ? x4[1] : make_float4(0.f, 0.f, 0.f, 0.f);
+          xs[g][0] = a.x; xs[g][1] = a.y; xs[g][2] = a.z; xs[g][3] = a.w;
+          xs[g][4] = b.x; xs[g][5] = b.y; xs[g][6] = b.z; xs[g][7] = b.w;
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) xs[g][k] = k0 + k < n ? x[k0 + k] : 0.f;
+        }
       }
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (k0 + k < n) s = (k0 + k == 0) ? (double)xs[k] : s + xs[k];
+      for (int g = 0; g < kWires; ++g)
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (k0 + k < n) s[g] = (k0 + k == 0) ? (double)xs[g][k] : s[g] + xs[g][k];
     }
-    o[w * J + j] = (float)s;
+#pragma unroll
+    for (int g = 0; g < kWires; ++g) {
+      const int64_t w = w0 + g * step;
+      if (w < W) o[w * J + j] = (float)s[g];
+    }
   }
 }
 
@@ -257,11 +272,12 @@ hipError_t launch_bin_ticks(const PlaneTable& in, const PlaneTable& out, int tic
     if (in.p[i].n_wires > wmax) wmax = in.p[i].n_wires;
   }
   if (jmax <= 0 || in.n <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((jmax + 255) / 256), (unsigned)(wmax < 65535 ? wmax : 65535),
-                  (unsigned)in.n);
   bool vec4 = ticks_per_column % 4 == 0;
   for (int i = 0; i < in.n; ++i)
     vec4 = vec4 && (reinterpret_cast<uintptr_t>(in.p[i].image) & 15) == 0 && in.p[i].n_ticks % 4 == 0;
+  const int64_t wy = vec4 ? (wmax + 3) / 4 : wmax;   // wires per thread and pass: 4 or 1
+  const dim3 grid((unsigned)((jmax + 255) / 256), (unsigned)(wy < 65535 ? wy : 65535),
+                  (unsigned)in.n);
   if (vec4) return launch_kernel(bin_ticks_kernel<true>, grid, dim3(256), 0, stream, in, out, ticks_per_column);
   return launch_kernel(bin_ticks_kernel<false>, grid, dim3(256), 0, stream, in, out, ticks_per_column);
 }
