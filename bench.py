@@ -75,12 +75,12 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed steps (default 100; 20 for --config 5 and --find-hits)")
+                    help="timed steps (default 100; 20 for --config 5)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps before them (default 100, about 0.14 s of the event: under "
                          "full load the chip's power controller settles over the first 30-40 ms, "
                          "during which the 16-bit fused kernel runs 5-15 %% slower; 3 for "
-                         "--config 5 and --find-hits)")
+                         "--config 5, whose steps are whole serving runs)")
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--precision", default="fp16", choices=["fp32", "bf16", "fp16", "fp8"])
     ap.add_argument("--batch", type=int, default=16384, help="config 4 batch size")
@@ -128,7 +128,7 @@ def parse():
                     help="first run 3 device-to-device copies of MIB MiB (a plain copy kernel of "
                          "known size, to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
-    light = args.config == 5 or args.find_hits is not None
+    light = args.config == 5 and args.find_hits is None
     if args.steps is None:
         args.steps = 20 if light else 100
     if args.warmup is None:
