@@ -462,13 +462,18 @@ __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_kernel(
 // sees the same operands in the same order as in the tiles above, and the
 // reduction over position groups is the same: a patch's sums are bit for bit
 // those of the other tile shapes.
+// With kParts = 2 or 4 the 128 FC1 outputs are shared by that many blocks
+// (each wave takes 4 / kParts of the 16-output tiles): more blocks, each
+// streaming a part of the position range's weights, for batches that would
+// leave CUs idle; every block computes the conv.
 constexpr int kThinRows = 11;                 // input rows of one position range, at most
-template <int kBt>
+template <int kBt, int kParts>
 struct Thin {
   static constexpr int kTiles = kBt / 16;
+  static constexpr int kMTw = kMT / kParts;                // 16-output tiles per wave
   static constexpr int kSlot = kBt * kRP;                  // dwords per staged row
   // the reduction: per output half, 3 tiles from the other groups per accumulator tile
-  static constexpr int kRed = kNHalves * kMT * kTiles * (kKGroups - 1) * 4 * 64;
+  static constexpr int kRed = kNHalves * kMTw * kTiles * (kKGroups - 1) * 4 * 64;
   // one row slot more than a range needs: the loop reads the window of the
   // pair after its last one (the result is never used), which may lie one row lower
   static constexpr int kRowsDw = (kThinRows + 1) * kSlot;
@@ -476,6 +481,7 @@ struct Thin {
   static constexpr int kRowChunks = kBt * 6;               // 16 B chunks per staged row
   static constexpr int kPer = (kThinRows * kRowChunks + kThreads - 1) / kThreads;
   static_assert(kTiles >= 1 && kTiles <= 2, "1 or 2 patch tiles");
+  static_assert(kParts == 1 || kParts == 2 || kParts == 4, "whole, half or quarter of the outputs");
 };
 
 // input rows a position range spans, at most, over the ranges of `splits`
@@ -490,13 +496,13 @@ constexpr int thin_rows_needed(int splits) {
   return most;
 }
 
-template <bool kFp16, int kSplits, int kBt, class In>
+template <bool kFp16, int kSplits, int kBt, int kParts, class In>
 __device__ __forceinline__ void thin_block(
-    uint32_t* lds, int split, int64_t p_base, const In* __restrict__ patches, int64_t n,
-    const uint4* __restrict__ w1p, const uint4* __restrict__ convp, float* __restrict__ part,
-    int64_t row0, int64_t n_total) {
-  using T = Thin<kBt>;
-  constexpr int kTiles = T::kTiles, kSlot = T::kSlot;
+    uint32_t* lds, int split, int opart, int64_t p_base, const In* __restrict__ patches,
+    int64_t n, const uint4* __restrict__ w1p, const uint4* __restrict__ convp,
+    float* __restrict__ part, int64_t row0, int64_t n_total) {
+  using T = Thin<kBt, kParts>;
+  constexpr int kTiles = T::kTiles, kSlot = T::kSlot, kMTw = T::kMTw;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -572,23 +578,24 @@ __device__ __forceinline__ void thin_block(
   };
   const __amdgpu_buffer_rsrc_t w1r = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint4*>(w1p), (short)0, (int)(kFc1Frags * 16), 0x00020000);
-  const int voff = lane * 16 + nh * kMT * 1024;
+  const int ot0 = (opart * kNHalves + nh) * kMTw;           // the wave's first output tile
+  const int voff = lane * 16 + ot0 * 1024;
   auto load_one = [&](int P, int q, int m) {
     return __builtin_bit_cast(
         uint4, __builtin_amdgcn_raw_buffer_load_b128(w1r, voff + m * 1024, (P * 3 + q) * 8 * 1024, 0));
   };
 
-  floatx4 acc[kMT][kTiles];
+  floatx4 acc[kMTw][kTiles];
 #pragma unroll
-  for (int m = 0; m < kMT; ++m)
+  for (int m = 0; m < kMTw; ++m)
 #pragma unroll
     for (int i = 0; i < kTiles; ++i) acc[m][i] = (floatx4){0.f, 0.f, 0.f, 0.f};
   // FC1 weights: 3 register sets, set q for K-step q of a pair, each reloaded
   // for the next pair as soon as its MFMAs have issued (three K-steps ahead:
   // with one or two patch tiles a K-step is short)
-  uint4 w[3][kMT], win[kTiles], own[kTiles];
+  uint4 w[3][kMTw], win[kTiles], own[kTiles];
 #pragma unroll
-  for (int m = 0; m < kMT; ++m) {
+  for (int m = 0; m < kMTw; ++m) {
     w[0][m] = load_one(P0 + kg, 0, m);
     w[1][m] = load_one(P0 + kg, 1, m);
     w[2][m] = load_one(P0 + kg, 2, m);
@@ -608,7 +615,7 @@ __device__ __forceinline__ void thin_block(
       const int nq = (q + 1) % 3;            // the next K-step
       // FC1 of K-step q (past the end of the weights the reload reads 0)
 #pragma unroll
-      for (int m = 0; m < kMT; ++m) {
+      for (int m = 0; m < kMTw; ++m) {
 #pragma unroll
         for (int i = 0; i < kTiles; ++i) acc[m][i] = Op::mfma(w[q][m], own[i], acc[m][i]);
         w[q][m] = load_one(P + kKGroups, q, m);
@@ -630,11 +637,15 @@ __device__ __forceinline__ void thin_block(
 
   // ---- the fixed-order reduction of the tiles above: (g0 + g2) + (g1 + g3),
   // each position group finishing a quarter of its output half's tiles, as in
-  // the tiles above
+  // the tiles above (with 2 tiles per half groups 0 and 2 finish one each,
+  // with 1 group 0 finishes it)
   __syncthreads();                           // every wave is done with the rows
-  constexpr int kSlots = kMT * kTiles;
-  constexpr int kPer = kSlots / kKGroups;
-  static_assert(kSlots % kKGroups == 0, "whole quarters");
+  constexpr int kSlots = kMTw * kTiles;
+  static_assert(kSlots % kKGroups == 0 || kKGroups % kSlots == 0, "tiles spread evenly");
+  // the position group that finishes slot q
+  constexpr auto owner = [](int q) {
+    return kSlots >= kKGroups ? q / (kSlots / kKGroups) : q * (kKGroups / kSlots);
+  };
   floatx4* red = reinterpret_cast<floatx4*>(lds);
   auto entry = [&](int q, int src) { return ((nh * kSlots + q) * (kKGroups - 1) + src) * 64 + lane; };
   auto tile = [&](auto qc) -> floatx4& {
@@ -642,14 +653,14 @@ __device__ __forceinline__ void thin_block(
     return acc[q / kTiles][q % kTiles];
   };
   static_for<kSlots>([&](auto qc) {
-    constexpr int o = decltype(qc)::value / kPer;
+    constexpr int o = owner(decltype(qc)::value);
     if (kg != o) red[entry(decltype(qc)::value, kg - (kg > o ? 1 : 0))] = tile(qc);
   });
   __syncthreads();
 
   float* dst = part + ((int64_t)split * n_total + row0 + p_base) * kFc1Out;
   static_for<kSlots>([&](auto qc) {
-    constexpr int q = decltype(qc)::value, o = q / kPer, m = q / kTiles, i = q % kTiles;
+    constexpr int q = decltype(qc)::value, o = owner(q), m = q / kTiles, i = q % kTiles;
     if (kg == o) {
       floatx4 v[kKGroups];
 #pragma unroll
@@ -657,23 +668,26 @@ __device__ __forceinline__ void thin_block(
         v[g] = (g == o) ? tile(qc) : red[entry(q, g - (g > o ? 1 : 0))];
       const floatx4 sum = (v[0] + v[2]) + (v[1] + v[3]);
       const int64_t po = (int64_t)i * 16 + col;
-      const int out = 16 * (nh * kMT + m) + 4 * grp;
+      const int out = 16 * (ot0 + m) + 4 * grp;
       if (p_base + po < n)
         __builtin_nontemporal_store(sum, reinterpret_cast<floatx4*>(dst + po * kFc1Out + out));
     }
   });
 }
 
-template <bool kFp16, int kSplits, int kBt, class In>
+// Block b: split b % kSplits, then output part, then patch tile.
+template <bool kFp16, int kSplits, int kBt, int kParts, class In>
 __global__ __launch_bounds__(kThreads, 1) void conv_fc1_16_thin_kernel(
     const In* __restrict__ patches, int64_t n, const uint4* __restrict__ w1p,
     const uint4* __restrict__ convp, float* __restrict__ part, int64_t row0, int64_t n_total) {
   static_assert(thin_rows_needed(kSplits) <= kThinRows, "a position range's rows fit the stage");
-  __shared__ __attribute__((aligned(16))) uint32_t lds[Thin<kBt>::kLdsDwords];
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Thin<kBt, kParts>::kLdsDwords];
   const int split = blockIdx.x % kSplits;
-  const int64_t t = blockIdx.x / kSplits;
-  thin_block<kFp16, kSplits, kBt, In>(lds, split, t * kBt, patches, n, w1p, convp, part, row0,
-                                      n_total);
+  const int64_t r = blockIdx.x / kSplits;
+  const int opart = (int)(r % kParts);
+  const int64_t t = r / kParts;
+  thin_block<kFp16, kSplits, kBt, kParts, In>(lds, split, opart, t * kBt, patches, n, w1p, convp,
+                                              part, row0, n_total);
 }
 
 constexpr int kSplits16 = 8;
@@ -725,6 +739,17 @@ int conv_fc1_16_thin_tile(int64_t n, int cus) {
   return 0;
 }
 
+// Output parts of a 16-patch thin tile: the most (4, 2 or 1) whose blocks
+// still fit one round of the CUs.  (Two blocks per CU were slower than one
+// block with all the outputs: 512 patches 54.5 against 51.5 us per call,
+// 1,024 in 32-patch tiles 71.6 against 60.9 us.)
+int conv_fc1_16_thin_parts(int64_t n, int cus, int thin) {
+  if (thin != 16) return 1;
+  const int64_t blocks = (n + thin - 1) / thin * kSplits16;
+  if (4 * blocks <= cus) return 4;
+  return 2 * blocks <= cus ? 2 : 1;
+}
+
 template <bool kFp16, class In>
 hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_total,
                         const uint4* w1p, const uint4* convp, float* part, hipStream_t stream) {
@@ -734,12 +759,16 @@ hipError_t launch_typed(const In* patches, int64_t n, int64_t row0, int64_t n_to
   if (e != hipSuccess) return e;
   const int thin = conv_fc1_16_thin_tile(n, cus);
   if (thin) {
-    const dim3 grid((unsigned)((n + thin - 1) / thin * kSplits16));
-    if (thin == 16)
-      return launch_kernel(conv_fc1_16_thin_kernel<kFp16, kSplits16, 16, In>, grid, dim3(kThreads),
-                           0, stream, patches, n, w1p, convp, part, row0, n_total);
-    return launch_kernel(conv_fc1_16_thin_kernel<kFp16, kSplits16, 32, In>, grid, dim3(kThreads), 0,
-                         stream, patches, n, w1p, convp, part, row0, n_total);
+    const int parts = conv_fc1_16_thin_parts(n, cus, thin);
+    const dim3 grid((unsigned)((n + thin - 1) / thin * kSplits16 * parts));
+    auto go = [&](auto kernel) {
+      return launch_kernel(kernel, grid, dim3(kThreads), 0, stream, patches, n, w1p, convp, part,
+                           row0, n_total);
+    };
+    if (thin == 32) return go(conv_fc1_16_thin_kernel<kFp16, kSplits16, 32, 1, In>);
+    if (parts == 4) return go(conv_fc1_16_thin_kernel<kFp16, kSplits16, 16, 4, In>);
+    return parts == 2 ? go(conv_fc1_16_thin_kernel<kFp16, kSplits16, 16, 2, In>)
+                      : go(conv_fc1_16_thin_kernel<kFp16, kSplits16, 16, 1, In>);
   }
   int64_t n_big = 0, n_mid = 0;
   conv_fc1_16_tiles(n, cus, &n_big, &n_mid);

@@ -179,6 +179,7 @@ int conv_fc1_16_splits();
 // patches, conv_fc1_16_thin_tile, runs those instead).
 void conv_fc1_16_tiles(int64_t n, int cus, int64_t* n_big, int64_t* n_mid);
 int conv_fc1_16_thin_tile(int64_t n, int cus);
+int conv_fc1_16_thin_parts(int64_t n, int cus, int thin);
 hipError_t launch_conv_fc1_16(bool fp16, const void* patches, bool f32_in, int64_t n, int64_t row0,
                               int64_t n_total, const uint4* w1p, const uint4* convp,
                               float* part, hipStream_t stream);

@@ -361,7 +361,8 @@ def test_tile_shapes_give_the_same_bits(pid, handles, prec):
 
     On a 256-CU device the 16-bit paths run 4,196 patches as 32 tiles of 96
     and 18 of 64; 3,073 and 4,000 patches as tiles of 64 only; up to 512
-    patches in thin tiles of 16 and up to 1,024 in thin tiles of 32.  The fp32
+    patches in thin tiles of 16 (whose outputs are shared by 4 blocks up to
+    128 patches and by 2 up to 256) and up to 1,024 in thin tiles of 32.  The fp32
     path runs 4,196 patches as 64 tiles of 64 plus 4 of 32.  The same patches
     classified in other batches land in other tiles and tile shapes, and must
     give the same bits."""
@@ -370,7 +371,8 @@ def test_tile_shapes_give_the_same_bits(pid, handles, prec):
     say(f"tile shapes {prec}")
     full = pid.pointid_classify_patches(h, t(P)).cpu().numpy().view(np.uint32)
     for lo, hi in [(4096, 4196), (0, 96), (4000, 4196), (1, 2), (4195, 4196), (100, 3173),
-                   (0, 4000), (0, 512), (96, 1096), (3000, 3513)]:
+                   (0, 4000), (0, 512), (96, 1096), (3000, 3513), (7, 150), (200, 456),
+                   (3940, 4069)]:
         part = pid.pointid_classify_patches(h, t(P[lo:hi])).cpu().numpy().view(np.uint32)
         assert np.array_equal(part, full[lo:hi]), f"patches {lo}:{hi}"
 
@@ -378,7 +380,8 @@ def test_tile_shapes_give_the_same_bits(pid, handles, prec):
 @pytest.mark.parametrize("prec", ["bf16", "fp16"])
 def test_schedule_boundaries_give_the_same_bits(pid, handles, prec):
     """Batch sizes on both sides of every change of tile schedule on a 256-CU
-    device (thin tiles of 16 up to 512 patches and of 32 up to 1,024, one round
+    device (thin tiles of 16 up to 512 patches, their outputs shared by 4
+    blocks up to 128 and by 2 up to 256, and of 32 up to 1,024, one round
     of 64-patch tiles up to 2,048, one round of 96 up to 3,072, then rounds of
     64 or of 96 and 64) give the bits the same patches get in one batch of
     6,200 (32 tiles of 96 and 49 of 64)."""
@@ -386,7 +389,7 @@ def test_schedule_boundaries_give_the_same_bits(pid, handles, prec):
     P = synth.config4_patches(6200, seed=77)
     say(f"schedule boundaries {prec}")
     full = pid.pointid_classify_patches(h, t(P)).cpu().numpy().view(np.uint32)
-    for size in (512, 513, 1024, 1025, 2048, 2049, 3072, 3073, 6143, 6144):
+    for size in (128, 129, 256, 257, 512, 513, 1024, 1025, 2048, 2049, 3072, 3073, 6143, 6144):
         lo = (size * 7) % (6200 - size + 1)
         part = pid.pointid_classify_patches(h, t(P[lo:lo + size])).cpu().numpy().view(np.uint32)
         assert np.array_equal(part, full[lo:lo + size]), f"{size} patches at {lo}"
